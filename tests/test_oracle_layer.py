@@ -1,0 +1,258 @@
+"""Pins of the oracle's sparse-layer arithmetic against references outside it.
+
+Forward and both backward products: the fixed fan-in layer is exactly a dense
+layer whose weight matrix has the ELLPACK support (Sec. 2.2), so a float64
+dense masked matmul and torch autograd through it give the same numbers up to
+rounding.  BCE: closed forms and torch's binary_cross_entropy_with_logits.
+Finite differences pin the gradients independently of autograd.  Adam: the
+torch.optim implementations.  None of these references shares code with the
+oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2411_03171_amd import synth
+
+
+def dense_mask(W, I, d):
+    L, k = W.shape
+    M = np.zeros((L, d))
+    M[np.arange(L)[:, None], I] = W
+    return M
+
+
+def tiny_case(seed, B=5, d=11, L=9, k=4, bias=True):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((B, d))
+    W = rng.uniform(-1, 1, (L, k))
+    I = synth.gen_indices(rng, L, k, d)
+    # shuffle slots so that indices are not sorted (the oracle must not rely on order)
+    perm = rng.permuted(np.tile(np.arange(k), (L, 1)), axis=1)
+    I = np.take_along_axis(I, perm, axis=1)
+    b = rng.standard_normal(L) if bias else None
+    off, lab = synth.gen_targets(rng, B, L, 2.5, 1.1)
+    return X, W, I, b, off, lab
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_forward_equals_dense_masked_matmul(oracle, seed):
+    X, W, I, b, _, _ = tiny_case(seed)
+    z = oracle.forward(X, W, I, b)
+    ref = X @ dense_mask(W, I, X.shape[1]).T + b
+    np.testing.assert_allclose(z, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_forward_full_fanin_is_dense_layer(oracle):
+    rng = np.random.default_rng(1)
+    B, d, L = 4, 6, 7
+    X = rng.standard_normal((B, d))
+    W = rng.standard_normal((L, d))
+    I = np.tile(np.arange(d, dtype=np.int32), (L, 1))
+    z = oracle.forward(X, W, I, None)
+    np.testing.assert_allclose(z, X @ W.T, rtol=1e-12)
+
+
+def test_forward_repeated_column_counts_each_slot(oracle):
+    # one column used by several rows and slots; exact small-integer arithmetic
+    X = np.array([[1.0, 2.0, 4.0]])
+    W = np.array([[1.0, 10.0], [100.0, 1000.0]])
+    I = np.array([[2, 0], [1, 2]], dtype=np.int32)
+    z = oracle.forward(X, W, I, np.array([0.5, -0.5]))
+    assert z.tolist() == [[0.5 + 4 + 10, -0.5 + 200 + 4000]]
+
+
+def test_targets_dense_dedups(oracle):
+    off = np.array([0, 3, 3, 5])
+    lab = np.array([2, 2, 0, 1, 4], dtype=np.int32)
+    y = oracle.targets_dense(3, 5, off, lab)
+    assert y.tolist() == [[1, 0, 1, 0, 0], [0, 0, 0, 0, 0], [0, 1, 0, 0, 1]]
+
+
+# -------------------------------------------------------------------- BCE
+
+def test_bce_closed_forms(oracle):
+    z = np.array([0.0, 0.0, 2.0, -3.0, 30.0, -30.0, 100.0, -100.0, 1000.0])
+    y = np.array([0, 1, 1, 0, 0, 1, 1, 0, 0], dtype=np.uint8)
+    s = 0.25
+    loss, g = oracle.bce(z, y, s)
+    softplus = lambda t: np.log1p(np.exp(-abs(t))) + max(t, 0.0)
+    terms = [np.log(2), np.log(2), softplus(-2.0), softplus(-3.0), softplus(30.0),
+             softplus(30.0), softplus(-100.0), softplus(-100.0), 1000.0]
+    assert np.isfinite(loss)
+    np.testing.assert_allclose(loss, s * sum(terms), rtol=1e-14)
+    sig = 1 / (1 + np.exp(-z))
+    np.testing.assert_allclose(g, s * (sig - y), rtol=1e-14, atol=1e-300)
+    assert g[0] == s * 0.5 and g[1] == -s * 0.5
+
+
+def test_bce_matches_torch(oracle):
+    rng = np.random.default_rng(3)
+    z = rng.standard_normal(1000) * 5
+    y = (rng.random(1000) < 0.1).astype(np.uint8)
+    loss, g = oracle.bce(z, y, 1 / 7)
+    zt = torch.tensor(z, requires_grad=True)
+    lt = torch.nn.functional.binary_cross_entropy_with_logits(
+        zt, torch.tensor(y, dtype=torch.float64), reduction="sum") / 7
+    lt.backward()
+    np.testing.assert_allclose(loss, lt.item(), rtol=1e-13)
+    np.testing.assert_allclose(g, zt.grad.numpy(), rtol=1e-12, atol=1e-15)
+
+
+# -------------------------------------------------------------- gradients
+
+def torch_dense_reference(X, W, I, b, off, lab, s):
+    B, d = X.shape
+    L, k = W.shape
+    y = np.zeros((B, L))
+    for bb in range(B):
+        y[bb, lab[off[bb]:off[bb + 1]]] = 1
+    Xt = torch.tensor(X, requires_grad=True)
+    Mt = torch.tensor(dense_mask(W, I, d), requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    z = Xt @ Mt.T + bt
+    loss = torch.nn.functional.binary_cross_entropy_with_logits(
+        z, torch.tensor(y), reduction="sum") * s
+    loss.backward()
+    dM = Mt.grad.numpy()
+    dW = dM[np.arange(L)[:, None], I]
+    return loss.item(), dW, bt.grad.numpy(), Xt.grad.numpy()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_backward_matches_autograd_of_dense_masked_layer(oracle, seed):
+    X, W, I, b, off, lab = tiny_case(seed, B=6, d=13, L=10, k=5)
+    s = 1 / 6
+    r = oracle.loss_and_grads(X, W, I, b, off, lab, s)
+    loss, dW, db, dX = torch_dense_reference(X, W, I, b, off, lab, s)
+    np.testing.assert_allclose(r["loss"], loss, rtol=1e-13)
+    np.testing.assert_allclose(r["dW"], dW, rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(r["dbias"], db, rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(r["dX"], dX, rtol=1e-11, atol=1e-14)
+
+
+def test_gradients_by_central_differences(oracle):
+    X, W, I, b, off, lab = tiny_case(11, B=4, d=9, L=7, k=3)
+    s = 0.25
+    r = oracle.loss_and_grads(X, W, I, b, off, lab, s)
+    h = 1e-6
+
+    def f(Xv=X, Wv=W, bv=b):
+        return oracle.loss_and_grads(Xv, Wv, I, bv, off, lab, s)["loss"]
+
+    rng = np.random.default_rng(0)
+    for _ in range(6):
+        l, j = rng.integers(7), rng.integers(3)
+        Wp, Wm = W.copy(), W.copy()
+        Wp[l, j] += h
+        Wm[l, j] -= h
+        fd = (f(Wv=Wp) - f(Wv=Wm)) / (2 * h)
+        assert abs(fd - r["dW"][l, j]) < 1e-7 * max(1.0, abs(fd))
+        bb, i = rng.integers(4), rng.integers(9)
+        Xp, Xm = X.copy(), X.copy()
+        Xp[bb, i] += h
+        Xm[bb, i] -= h
+        fd = (f(Xv=Xp) - f(Xv=Xm)) / (2 * h)
+        assert abs(fd - r["dX"][bb, i]) < 1e-7 * max(1.0, abs(fd))
+        bp, bm = b.copy(), b.copy()
+        bp[l] += h
+        bm[l] -= h
+        fd = (f(bv=bp) - f(bv=bm)) / (2 * h)
+        assert abs(fd - r["dbias"][l]) < 1e-7 * max(1.0, abs(fd))
+
+
+def test_dx_unused_column_is_zero(oracle):
+    X, W, I, b, off, lab = tiny_case(2, B=3, d=20, L=3, k=2)
+    r = oracle.loss_and_grads(X, W, I, b, off, lab, 1 / 3)
+    unused = np.setdiff1d(np.arange(20), I.ravel())
+    assert unused.size > 0
+    assert np.all(r["dX"][:, unused] == 0.0)
+
+
+def test_euler_identity_for_dx(oracle):
+    # sum_i X[b,i] dX[b,i] = sum_l g[b,l] (z[b,l] - bias[l]): the layer is linear in X
+    X, W, I, b, off, lab = tiny_case(4, B=5, d=12, L=8, k=4)
+    r = oracle.loss_and_grads(X, W, I, b, off, lab, 0.2)
+    lhs = (X * r["dX"]).sum(axis=1)
+    rhs = (r["g"] * (r["z"] - b)).sum(axis=1)
+    np.testing.assert_allclose(lhs, rhs, rtol=1e-12)
+
+
+# ------------------------------------------------------------------ Adam
+
+@pytest.mark.parametrize("wd", [0.0, 1e-2])
+def test_adam_matches_torch(oracle, wd):
+    rng = np.random.default_rng(5)
+    p0 = rng.standard_normal(50)
+    grads = [rng.standard_normal(50) for _ in range(4)]
+    pt = torch.tensor(p0.copy(), requires_grad=True)
+    opt = (torch.optim.AdamW([pt], lr=1e-2, betas=(0.9, 0.999), eps=1e-8, weight_decay=wd)
+           if wd else torch.optim.Adam([pt], lr=1e-2, betas=(0.9, 0.999), eps=1e-8))
+    p, m, v = p0.copy(), np.zeros(50), np.zeros(50)
+    for t, gr in enumerate(grads, start=1):
+        pt.grad = torch.tensor(gr)
+        opt.step()
+        p, m, v = oracle.adam(p, m, v, gr, t, lr=1e-2, wd=wd)
+    np.testing.assert_allclose(p, pt.detach().numpy(), rtol=1e-13, atol=1e-15)
+    st = opt.state[pt]
+    np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-13)
+    np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-13)
+
+
+def test_adam_first_step_closed_form(oracle):
+    g = np.array([0.5, -2.0, 1e-3, 0.0])
+    p, m, v = oracle.adam(np.ones(4), np.zeros(4), np.zeros(4), g, 1, lr=1e-3)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-14)
+    np.testing.assert_allclose(v, 0.001 * g * g, rtol=1e-14)
+    np.testing.assert_allclose(p, 1 - 1e-3 * g / (np.abs(g) + 1e-8), rtol=1e-14)
+
+
+def test_train_step_matches_torch_composition(oracle):
+    X, W, I, b, off, lab = tiny_case(7, B=4, d=10, L=6, k=3)
+    s = 0.25
+    L, k = W.shape
+    r = oracle.train_step(X, W, I, b, np.zeros((L, k)), np.zeros((L, k)), np.zeros(L),
+                          np.zeros(L), off, lab, s, t=1, lr=1e-2)
+    _, dW, db, dX = torch_dense_reference(X, W, I, b, off, lab, s)
+    Wt = torch.tensor(W.copy(), requires_grad=True)
+    bt = torch.tensor(b.copy(), requires_grad=True)
+    opt = torch.optim.Adam([Wt, bt], lr=1e-2)
+    Wt.grad, bt.grad = torch.tensor(dW), torch.tensor(db)
+    opt.step()
+    np.testing.assert_allclose(r["W"], Wt.detach().numpy(), rtol=1e-12)
+    np.testing.assert_allclose(r["bias"], bt.detach().numpy(), rtol=1e-12)
+    np.testing.assert_allclose(r["dX"], dX, rtol=1e-11, atol=1e-14)
+
+
+# ---------------------------------------------------------------- bf16
+
+def test_round_bf16_matches_torch(oracle):
+    rng = np.random.default_rng(9)
+    x = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32),
+        (rng.standard_normal(2000) * 1e-39).astype(np.float32),      # subnormals
+        np.array([3.3895314e38, 3.4e38, -3.4e38, 0.0, -0.0, 1e-45], dtype=np.float32),
+    ])
+    # exact halfway cases between two bf16 neighbours: low 16 bits == 0x8000
+    u = rng.integers(0x00800000, 0x7f000000, size=2000, dtype=np.uint32)
+    half = ((u & 0xFFFF0000) | 0x8000).view(np.float32)
+    x = np.concatenate([x, half, -half])
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = oracle.round_bf16(x.astype(np.float64))
+    assert np.array_equal(got, ref)
+
+
+def test_round_bf16_double_inputs():
+    import oracle
+    # a double just above a bf16 halfway point must round up even though its
+    # float32 rounding would sit exactly on the halfway point
+    x = 1.0 + 2.0 ** -8 + 2.0 ** -40
+    assert oracle.round_bf16(np.array([x]))[0] == 0x3F81
+    assert oracle.round_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 0x3F80   # tie -> even
+
+
+def test_synth_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal(5000).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(synth.f32_to_bf16_bits(x), ref)
