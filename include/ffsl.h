@@ -1,0 +1,197 @@
+/*
+ * ffsl.h -- C ABI of libffsl, the MI355X (gfx950) library for the fixed
+ * fan-in sparse classification layer of "Navigating Extremes: Dynamic
+ * Sparsity in Large Output Spaces" (NeurIPS 2024).
+ *
+ * The layer (Sec. 2.2): L label rows, each holding exactly k weights W[l,j]
+ * at k distinct input columns I[l,j] in [0,d) -- ELLPACK storage without
+ * padding.  Scores are one-vs-all logits of an input batch X[B,d] (Sec. 2.1);
+ * the training step is BCE-with-logits (Appendix "Hyperparameter Settings"),
+ * both backward products, Adam, and every Delta-T steps a SET
+ * prune-and-regrow that rewrites W and I in place (Sec. 2.1).
+ *
+ * Conventions for every entry point
+ *   - All array arguments are DEVICE pointers unless stated otherwise, and
+ *     every array is dense row-major: X[b*d+i], W[l*k+j], I[l*k+j],
+ *     logits[b*L+l].  The caller owns all memory; the library never
+ *     allocates device memory.  Scratch lives in the caller's workspace.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued asynchronously; results are valid after the caller
+ *     synchronises the stream.  No entry point synchronises.
+ *   - Return value: FFSL_OK (0) or a negative ffsl_status.  Arguments are
+ *     validated on the host before anything is enqueued; on error nothing is
+ *     enqueued and ffsl_last_error() (per thread) describes the problem.
+ *     Device-side conditions (SET rows that exhaust their draw budget,
+ *     out-of-range indices found by ffsl_validate_indices) are reported
+ *     through optional device counters instead.
+ *   - A layer handle may be used from one host thread at a time, and the
+ *     calls that share one workspace must be ordered (same stream, or
+ *     synchronised): they reuse its scratch regions.
+ */
+#ifndef FFSL_H
+#define FFSL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* symbols of the shared library (it is built with hidden visibility) */
+#define FFSL_API __attribute__((visibility("default")))
+
+typedef enum {
+    FFSL_OK = 0,
+    FFSL_EINVAL = -1,       /* bad argument (null pointer, size, range)     */
+    FFSL_EUNSUPPORTED = -2, /* valid but outside what the kernels support   */
+    FFSL_EHIP = -3          /* a HIP runtime call or kernel launch failed   */
+} ffsl_status;
+
+typedef enum {
+    FFSL_F32 = 0,  /* IEEE binary32                                         */
+    FFSL_BF16 = 1  /* bfloat16 bit patterns (uint16); arithmetic in fp32    */
+} ffsl_dtype;
+
+/* flags */
+#define FFSL_ACCUM_DX 1u   /* add into dX_out instead of overwriting it      */
+#define FFSL_ACCUM_LOSS 2u /* add into *loss_out instead of overwriting it   */
+
+/* Limits of this build. */
+#define FFSL_MAX_K 128         /* fan-in                                    */
+#define FFSL_MAX_D 16384       /* input width                               */
+#define FFSL_MAX_B 1024        /* batch size                                */
+
+typedef struct ffsl_layer ffsl_layer;
+
+/* Message of the last failed call on this host thread ("" if none). */
+FFSL_API const char *ffsl_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+FFSL_API int ffsl_version(void);
+
+/* Bytes of device workspace a layer of this shape needs for batches of up to
+ * B_max samples with up to nnz_max positive (sample, label) pairs per batch.
+ * Returns 0 for invalid shapes. */
+FFSL_API size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max,
+                            int32_t nnz_max);
+
+/* Create a handle over caller-owned layer state (Sec. 2.2 storage; Sec. 2.2
+ * notes that gradient and both Adam moments share the weights' index
+ * structure, so m, v (and dW) are [L,k] arrays aligned with W and I).
+ *   L, d, k     labels, input width, fan-in (1 <= k <= min(d, FFSL_MAX_K))
+ *   value_dtype FFSL_F32 or FFSL_BF16: type of W and of every X passed later
+ *   W           [L,k] weights (value_dtype)
+ *   I           [L,k] int32 input columns, distinct within a row, in [0,d)
+ *   bias        [L] fp32, nullable (no bias term)
+ *   m, v        [L,k] fp32 Adam moments of W
+ *   bias_m, bias_v  [L] fp32 Adam moments of bias (required iff bias)
+ *   dW, dbias   [L,k] / [L] fp32 gradient buffers of the unfused path,
+ *               nullable (then ffsl_backward/ffsl_adam_step are unavailable)
+ *   workspace   device scratch of at least ffsl_workspace_bytes(...) bytes,
+ *               256-byte aligned
+ * The handle stores the pointers and shapes only; it owns no device memory.
+ * Errors: FFSL_EINVAL for null required pointers, bad shapes or a short
+ * workspace. */
+FFSL_API int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k,
+                      int32_t value_dtype, void *W, int32_t *I, float *bias,
+                      float *m, float *v, float *bias_m, float *bias_v,
+                      float *dW, float *dbias, void *workspace,
+                      size_t workspace_bytes, int32_t B_max, int32_t nnz_max);
+
+FFSL_API int ffsl_destroy_layer(ffsl_layer *layer);
+
+/* Gathered forward and BCE loss (Sec. 2.2; Appendix "Hyperparameter
+ * Settings"):
+ *   z[b,l]  = bias[l] + sum_j W[l,j] * X[b, I[l,j]]
+ *   *loss_out (device fp32) = s * sum_{b,l} [max(z,0) - z*y + log1p(exp(-|z|))]
+ * with y[b,l] = 1 iff l is a positive of sample b.
+ *   X        [B,d] value_dtype, 1 <= B <= B_max
+ *   tgt_off  [B+1] int32 CSR offsets (tgt_off[0] = 0, non-decreasing,
+ *            tgt_off[B] = nnz); tgt_lab [nnz] int32 labels in [0,L);
+ *            repeated labels within a sample count once.  nnz <= nnz_max.
+ *            The contents are trusted: labels outside [0,L) are ignored.
+ *   s        loss scale (1/B averages over the batch)
+ *   logits_out  nullable fp32 [B,L]; when given the scores are written out
+ *            (for tests -- the training path never materialises them).
+ */
+FFSL_API int ffsl_forward_loss(ffsl_layer *layer, const void *X, int32_t B,
+                      const int32_t *tgt_off, const int32_t *tgt_lab,
+                      int32_t nnz, float s, float *loss_out, float *logits_out,
+                      uint32_t flags, void *stream);
+
+/* Both backward products (Sec. 2.2) of the BCE loss above, recomputing the
+ * scores in the same sweep:
+ *   g[b,l]   = s * (sigmoid(z[b,l]) - y[b,l])
+ *   dW[l,j]  = sum_b g[b,l] * X[b, I[l,j]]      -> layer dW  (fp32 [L,k])
+ *   dbias[l] = sum_b g[b,l]                     -> layer dbias (if bias)
+ *   dX[b,i]  = sum_{l,j: I[l,j]=i} g[b,l]*W[l,j] -> dX_out fp32 [B,d]
+ * dX_out is overwritten, or added into with FFSL_ACCUM_DX.  loss_out is
+ * nullable; when given the loss is written as in ffsl_forward_loss.
+ * Requires the layer's dW buffer. */
+FFSL_API int ffsl_backward(ffsl_layer *layer, const void *X, int32_t B,
+                  const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz,
+                  float s, float *loss_out, float *dX_out, uint32_t flags,
+                  void *stream);
+
+/* Adam / AdamW step (Appendix "Hyperparameter Settings": AdamW for the
+ * classifier) on W (from the layer's dW) and on the bias (from dbias):
+ *   p <- p*(1 - lr*wd);  m <- b1*m + (1-b1)*g;  v <- b2*v + (1-b2)*g^2
+ *   p <- p - lr * (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
+ * t >= 1 is the step number of this update.  Arithmetic in fp32; a bf16 W
+ * is written back rounded to nearest even.  Requires the layer's dW. */
+FFSL_API int ffsl_adam_step(ffsl_layer *layer, int64_t t, float lr, float beta1,
+                   float beta2, float eps, float wd, void *stream);
+
+/* One fused training step: forward, BCE, dW, dbias, dX and Adam in one
+ * streaming pass over the [L,k] arrays; the scores and dW never leave the
+ * chip.  Same semantics as ffsl_forward_loss + ffsl_backward +
+ * ffsl_adam_step with the same arguments (up to fp32 rounding order); the
+ * layer's dW/dbias buffers are neither needed nor written.  loss_out and
+ * dX_out are nullable. */
+FFSL_API int ffsl_train_step(ffsl_layer *layer, const void *X, int32_t B,
+                    const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz,
+                    float s, int64_t t, float lr, float beta1, float beta2,
+                    float eps, float wd, float *loss_out, float *dX_out,
+                    uint32_t flags, void *stream);
+
+/* SET prune-and-regrow (Sec. 2.1: magnitude pruning, random regrowth of as
+ * many inactive weights; Appendix "Hyperparameter Settings": random growth
+ * with zero initialisation), row by row so the fan-in stays exactly k:
+ *   n = floor(frac*k + 1e-9) slots per row with the smallest keys
+ *       (|W| bit pattern, slot) are pruned -- ties go to the smaller slot,
+ *       -0 ties +0, NaN ranks above +inf;
+ *   attempt a = 0,1,... takes 64-bit word (a mod 4) of
+ *       Philox4x64-10(counter = (l, set_round, a/4, 0),
+ *                     key = (seed, 0x5345545F52454752)),
+ *       maps it to column floor(word*d / 2^64) and accepts it if the row
+ *       did not hold it before pruning and it was not accepted already;
+ *   accepted columns fill the pruned slots in ascending slot order with
+ *       W = +0 and m = v = 0; all other slots keep their bits;
+ *   a row that has not found n columns after 64*k + 4096 attempts is left
+ *       unchanged and counted in *exhausted_out (nullable device int32,
+ *       added to).
+ *   pruned_mask_out  nullable uint8 [L,k]: 1 where a slot was regrown.
+ * Errors: FFSL_EINVAL if n > d - k (too few inactive columns). */
+FFSL_API int ffsl_set_update(ffsl_layer *layer, float frac, uint64_t seed,
+                    uint64_t set_round, uint8_t *pruned_mask_out,
+                    int32_t *exhausted_out, void *stream);
+
+/* Measurement hook: while both events are non-null, every sweep call
+ * (ffsl_forward_loss, ffsl_backward, ffsl_train_step) records `start`
+ * (a hipEvent_t) on its stream right before its main sweep kernel and `stop`
+ * right after it, so a caller can time that kernel alone with
+ * hipEventElapsedTime.  Pass NULLs to turn it off.  The handle keeps the
+ * event handles, not copies. */
+FFSL_API int ffsl_set_timing_events(ffsl_layer *layer, void *start, void *stop);
+
+/* Debug check of the index structure: adds to *bad_rows_out (device int32)
+ * the number of rows with an index outside [0,d) or a repeated index. */
+FFSL_API int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out,
+                          void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FFSL_H */

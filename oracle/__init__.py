@@ -58,7 +58,7 @@ def lib():
         L.ffslref_set_prune_count.argtypes = [i64, dbl]
         L.ffslref_set_prune_count.restype = i64
         L.ffslref_set_update.argtypes = [i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
-                                         dbl, u64, u64, ctypes.c_int]
+                                         dbl, u64, u64, ctypes.c_int, u64]
         L.ffslref_set_update.restype = i64
         L.ffslref_dense_gelu_fwd.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp]
         L.ffslref_dense_gelu_fwd.restype = None
@@ -195,8 +195,10 @@ def set_prune_count(k, frac):
     return int(lib().ffslref_set_prune_count(int(k), float(frac)))
 
 
-def set_update(Wbits, I, m, v, d, frac, seed, set_round, allow_regrow_pruned=False):
+def set_update(Wbits, I, m, v, d, frac, seed, set_round, allow_regrow_pruned=False, row0=0):
     """SET on copies of the state.  Wbits is uint16 (bf16) or uint32 (fp32).
+
+    The arrays may be a block of rows starting at layer row ``row0``.
 
     Returns (Wbits, I, m, v, mask, exhausted_rows).
     """
@@ -214,7 +216,8 @@ def set_update(Wbits, I, m, v, d, frac, seed, set_round, allow_regrow_pruned=Fal
     mask = np.empty((L, k), dtype=np.uint8)
     ex = lib().ffslref_set_update(L, int(d), k, wbits, _p(Wb), _p(Ic), _p(mc), _p(vc),
                                   _p(mask), float(frac), int(seed) & (2**64 - 1),
-                                  int(set_round) & (2**64 - 1), int(bool(allow_regrow_pruned)))
+                                  int(set_round) & (2**64 - 1), int(bool(allow_regrow_pruned)),
+                                  int(row0))
     if ex < 0:
         raise ValueError("invalid SET arguments")
     return Wb, Ic, mc, vc, mask, int(ex)

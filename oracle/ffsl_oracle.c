@@ -267,6 +267,8 @@ EXPORT void ffslref_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2],
  *   zero init = a regrown slot gets W = +0 (bits 0), m = v = 0, mask = 1.
  * The survivors' bits are untouched and the row is not re-sorted.
  *
+ * The arrays hold rows row0 .. row0+L-1 of the layer (row0 = 0 for the
+ * whole layer); the draw counter uses the layer's row number row0 + l.
  * W is given as bit patterns: wbits = 16 (bf16, uint16_t*) or 32 (fp32,
  * uint32_t*).  m, v, mask may be NULL.  Returns the number of exhausted rows,
  * or -1 for invalid arguments (n > d - k while the pruned columns are not
@@ -281,7 +283,8 @@ EXPORT int64_t ffslref_set_prune_count(int64_t k, double frac)
 EXPORT int64_t ffslref_set_update(int64_t L, int64_t d, int64_t k, int wbits,
                                   void *Wbits, int32_t *I, float *m, float *v,
                                   uint8_t *mask, double frac, uint64_t seed,
-                                  uint64_t set_round, int allow_regrow_pruned)
+                                  uint64_t set_round, int allow_regrow_pruned,
+                                  uint64_t row0)
 {
     int64_t n = ffslref_set_prune_count(k, frac);
     if (n < 0 || n > k || (wbits != 16 && wbits != 32))
@@ -330,7 +333,7 @@ EXPORT int64_t ffslref_set_update(int64_t L, int64_t d, int64_t k, int wbits,
         /* draw n new columns */
         int64_t got = 0;
         for (int64_t a = 0; a < cap && got < n; ++a) {
-            uint64_t ctr[4] = {(uint64_t)l, set_round, (uint64_t)(a / 4), 0};
+            uint64_t ctr[4] = {row0 + (uint64_t)l, set_round, (uint64_t)(a / 4), 0};
             uint64_t key[2] = {seed, SET_KEY_HI};
             uint64_t out[4];
             ffslref_philox4x64_10(ctr, key, out);

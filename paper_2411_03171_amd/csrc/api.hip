@@ -1,0 +1,300 @@
+// C ABI of libffsl: argument validation, workspace layout, dispatch.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+
+#include "ffsl_internal.h"
+
+struct ffsl_layer {
+    ffsl::Layer ly;
+};
+
+namespace ffsl {
+
+static thread_local std::string g_err;
+
+void set_error(const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+}
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int check_launch(const char *what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(FFSL_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
+    return FFSL_OK;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int max_parts_for(int num_cu) { return std::max(1, std::min(2 * num_cu, 1024)); }
+
+WsLayout ws_layout(int32_t d, int32_t B_max, int32_t nnz_max, int max_parts) {
+    WsLayout w{};
+    size_t off = 0;
+    w.loss_part = off;
+    off = align256(off + sizeof(float) * (size_t)max_parts);
+    w.tgt_b = off;
+    off = align256(off + sizeof(int32_t) * (size_t)std::max(nnz_max, 1));
+    w.dx_part = off;
+    off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)B_max * (size_t)d);
+    w.total = off;
+    return w;
+}
+
+static int device_cu_count(int *cu, int *dev) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    e = hipDeviceGetAttribute(cu, hipDeviceAttributeMultiprocessorCount, *dev);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
+    return FFSL_OK;
+}
+
+static int check_shape(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max) {
+    if (L < 1) return fail(FFSL_EINVAL, "L must be >= 1 (got %lld)", (long long)L);
+    if (d < 1 || d > FFSL_MAX_D) return fail(FFSL_EINVAL, "d must be in [1,%d] (got %d)", FFSL_MAX_D, d);
+    if (k < 1 || k > d || k > FFSL_MAX_K)
+        return fail(FFSL_EINVAL, "k must be in [1, min(d,%d)] (got k=%d, d=%d)", FFSL_MAX_K, k, d);
+    if (B_max < 1 || B_max > FFSL_MAX_B)
+        return fail(FFSL_EINVAL, "B_max must be in [1,%d] (got %d)", FFSL_MAX_B, B_max);
+    if (nnz_max < 0) return fail(FFSL_EINVAL, "nnz_max must be >= 0");
+    if (L > ((int64_t)1 << 40) / k) return fail(FFSL_EINVAL, "L*k too large");
+    return FFSL_OK;
+}
+
+static int check_batch(const Layer &ly, const void *X, int32_t B, const int32_t *off, const int32_t *lab,
+                       int32_t nnz) {
+    if (!X) return fail(FFSL_EINVAL, "X is null");
+    if (B < 1 || B > ly.B_max) return fail(FFSL_EINVAL, "B must be in [1,%d] (got %d)", ly.B_max, B);
+    if (!off) return fail(FFSL_EINVAL, "tgt_off is null");
+    if (nnz < 0 || nnz > ly.nnz_max)
+        return fail(FFSL_EINVAL, "nnz must be in [0,%d] (got %d)", ly.nnz_max, nnz);
+    if (nnz > 0 && !lab) return fail(FFSL_EINVAL, "tgt_lab is null");
+    return FFSL_OK;
+}
+
+static int check_adam(int64_t t, float lr, float b1, float b2, float eps, float wd, AdamParams *p) {
+    if (t < 1) return fail(FFSL_EINVAL, "Adam step t must be >= 1 (got %lld)", (long long)t);
+    if (!(b1 >= 0.f && b1 < 1.f) || !(b2 >= 0.f && b2 < 1.f))
+        return fail(FFSL_EINVAL, "betas must be in [0,1)");
+    if (!(eps >= 0.f) || !isfinite(lr) || !isfinite(wd)) return fail(FFSL_EINVAL, "bad lr/eps/wd");
+    p->lr = lr;
+    p->b1 = b1;
+    p->b2 = b2;
+    p->eps = eps;
+    p->wd = wd;
+    p->bc1 = (float)(1.0 - pow((double)b1, (double)t));
+    p->bc2 = (float)(1.0 - pow((double)b2, (double)t));
+    if (!(p->bc1 > 0.f) || !(p->bc2 > 0.f)) return fail(FFSL_EINVAL, "bias correction underflows");
+    return FFSL_OK;
+}
+
+}  // namespace ffsl
+
+using namespace ffsl;
+
+extern "C" {
+
+const char *ffsl_last_error(void) { return g_err.c_str(); }
+
+int ffsl_version(void) { return 100; }
+
+size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max) {
+    if (check_shape(L, d, k, B_max, nnz_max)) return 0;
+    int cu = 0, dev = 0;
+    if (device_cu_count(&cu, &dev)) return 0;
+    return ws_layout(d, B_max, nnz_max, max_parts_for(cu)).total;
+}
+
+int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype, void *W,
+                      int32_t *I, float *bias, float *m, float *v, float *bias_m, float *bias_v, float *dW,
+                      float *dbias, void *workspace, size_t workspace_bytes, int32_t B_max,
+                      int32_t nnz_max) {
+    g_err.clear();
+    if (!out) return fail(FFSL_EINVAL, "out is null");
+    *out = nullptr;
+    int rc = check_shape(L, d, k, B_max, nnz_max);
+    if (rc) return rc;
+    if (value_dtype != FFSL_F32 && value_dtype != FFSL_BF16)
+        return fail(FFSL_EINVAL, "value_dtype must be FFSL_F32 or FFSL_BF16");
+    if (!W || !I || !m || !v) return fail(FFSL_EINVAL, "W, I, m and v are required");
+    if (bias && (!bias_m || !bias_v)) return fail(FFSL_EINVAL, "bias needs bias_m and bias_v");
+    if (dbias && !bias) return fail(FFSL_EINVAL, "dbias given without bias");
+    if (!workspace) return fail(FFSL_EINVAL, "workspace is null");
+    if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(FFSL_EINVAL, "workspace must be 256-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(I) | reinterpret_cast<uintptr_t>(m) |
+         reinterpret_cast<uintptr_t>(v)) & 15)
+        return fail(FFSL_EINVAL, "W, I, m, v must be 16-byte aligned");
+    int cu = 0, dev = 0;
+    rc = device_cu_count(&cu, &dev);
+    if (rc) return rc;
+    const int parts = max_parts_for(cu);
+    const WsLayout wl = ws_layout(d, B_max, nnz_max, parts);
+    if (workspace_bytes < wl.total)
+        return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, wl.total);
+    ffsl_layer *h = new (std::nothrow) ffsl_layer;
+    if (!h) return fail(FFSL_EINVAL, "out of host memory");
+    Layer &ly = h->ly;
+    ly.L = L;
+    ly.d = d;
+    ly.k = k;
+    ly.vt = value_dtype;
+    ly.B_max = B_max;
+    ly.nnz_max = nnz_max;
+    ly.W = W;
+    ly.I = I;
+    ly.bias = bias;
+    ly.m = m;
+    ly.v = v;
+    ly.bm = bias_m;
+    ly.bv = bias_v;
+    ly.dW = dW;
+    ly.dbias = dbias;
+    ly.ws = static_cast<char *>(workspace);
+    ly.ws_bytes = workspace_bytes;
+    ly.num_cu = cu;
+    ly.max_parts = parts;
+    ly.device = dev;
+    ly.ev_start = nullptr;
+    ly.ev_stop = nullptr;
+    *out = h;
+    return FFSL_OK;
+}
+
+int ffsl_destroy_layer(ffsl_layer *layer) {
+    delete layer;
+    return FFSL_OK;
+}
+
+int ffsl_forward_loss(ffsl_layer *layer, const void *X, int32_t B, const int32_t *tgt_off,
+                      const int32_t *tgt_lab, int32_t nnz, float s, float *loss_out, float *logits_out,
+                      uint32_t flags, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    int rc = check_batch(layer->ly, X, B, tgt_off, tgt_lab, nnz);
+    if (rc) return rc;
+    if (!loss_out) return fail(FFSL_EINVAL, "loss_out is null");
+    SweepCall c{};
+    c.layer = &layer->ly;
+    c.X = X;
+    c.B = B;
+    c.tgt_off = tgt_off;
+    c.tgt_lab = tgt_lab;
+    c.nnz = nnz;
+    c.s = s;
+    c.mode = SWEEP_FWD;
+    c.loss_out = loss_out;
+    c.logits_out = logits_out;
+    c.flags = flags;
+    c.stream = static_cast<hipStream_t>(stream);
+    return launch_sweep(c);
+}
+
+int ffsl_backward(ffsl_layer *layer, const void *X, int32_t B, const int32_t *tgt_off, const int32_t *tgt_lab,
+                  int32_t nnz, float s, float *loss_out, float *dX_out, uint32_t flags, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    int rc = check_batch(layer->ly, X, B, tgt_off, tgt_lab, nnz);
+    if (rc) return rc;
+    if (!layer->ly.dW) return fail(FFSL_EINVAL, "layer was created without a dW buffer");
+    if (!dX_out) return fail(FFSL_EINVAL, "dX_out is null");
+    SweepCall c{};
+    c.layer = &layer->ly;
+    c.X = X;
+    c.B = B;
+    c.tgt_off = tgt_off;
+    c.tgt_lab = tgt_lab;
+    c.nnz = nnz;
+    c.s = s;
+    c.mode = SWEEP_BWD;
+    c.loss_out = loss_out;
+    c.dX_out = dX_out;
+    c.flags = flags;
+    c.stream = static_cast<hipStream_t>(stream);
+    return launch_sweep(c);
+}
+
+int ffsl_adam_step(ffsl_layer *layer, int64_t t, float lr, float beta1, float beta2, float eps, float wd,
+                   void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    if (!layer->ly.dW) return fail(FFSL_EINVAL, "layer was created without a dW buffer");
+    if (layer->ly.bias && !layer->ly.dbias) return fail(FFSL_EINVAL, "layer has a bias but no dbias buffer");
+    AdamParams p{};
+    int rc = check_adam(t, lr, beta1, beta2, eps, wd, &p);
+    if (rc) return rc;
+    return launch_adam(layer->ly, p, static_cast<hipStream_t>(stream));
+}
+
+int ffsl_train_step(ffsl_layer *layer, const void *X, int32_t B, const int32_t *tgt_off, const int32_t *tgt_lab,
+                    int32_t nnz, float s, int64_t t, float lr, float beta1, float beta2, float eps, float wd,
+                    float *loss_out, float *dX_out, uint32_t flags, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    int rc = check_batch(layer->ly, X, B, tgt_off, tgt_lab, nnz);
+    if (rc) return rc;
+    SweepCall c{};
+    rc = check_adam(t, lr, beta1, beta2, eps, wd, &c.adam);
+    if (rc) return rc;
+    c.layer = &layer->ly;
+    c.X = X;
+    c.B = B;
+    c.tgt_off = tgt_off;
+    c.tgt_lab = tgt_lab;
+    c.nnz = nnz;
+    c.s = s;
+    c.mode = SWEEP_FUSED;
+    c.loss_out = loss_out;
+    c.dX_out = dX_out;
+    c.flags = flags;
+    c.stream = static_cast<hipStream_t>(stream);
+    return launch_sweep(c);
+}
+
+int ffsl_set_update(ffsl_layer *layer, float frac, uint64_t seed, uint64_t set_round, uint8_t *pruned_mask_out,
+                    int32_t *exhausted_out, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    const Layer &ly = layer->ly;
+    if (!(frac >= 0.f && frac <= 1.f)) return fail(FFSL_EINVAL, "frac must be in [0,1] (got %g)", (double)frac);
+    const int32_t n = (int32_t)floor((double)frac * (double)ly.k + 1e-9);
+    if (n > ly.d - ly.k)
+        return fail(FFSL_EINVAL, "cannot regrow %d weights per row: only %d inactive columns", n, ly.d - ly.k);
+    if (n == 0 && !pruned_mask_out) return FFSL_OK;
+    return launch_set(ly, n, seed, set_round, pruned_mask_out, exhausted_out, static_cast<hipStream_t>(stream));
+}
+
+int ffsl_set_timing_events(ffsl_layer *layer, void *start, void *stop) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    if ((start == nullptr) != (stop == nullptr)) return fail(FFSL_EINVAL, "give both events or neither");
+    layer->ly.ev_start = static_cast<hipEvent_t>(start);
+    layer->ly.ev_stop = static_cast<hipEvent_t>(stop);
+    return FFSL_OK;
+}
+
+int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    if (!bad_rows_out) return fail(FFSL_EINVAL, "bad_rows_out is null");
+    return launch_validate(layer->ly, bad_rows_out, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+// Internal declarations of libffsl (HIP, gfx950).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/ffsl.h"
+
+namespace ffsl {
+
+// ---------------------------------------------------------------- layer
+
+struct Layer {
+    int64_t L;
+    int32_t d, k, vt, B_max, nnz_max;
+    void *W;
+    int32_t *I;
+    float *bias, *m, *v, *bm, *bv, *dW, *dbias;
+    char *ws;
+    size_t ws_bytes;
+    int num_cu;      // compute units of the device the layer was created on
+    int max_parts;   // per-workgroup partial buffers carved in the workspace
+    int device;
+    hipEvent_t ev_start, ev_stop;  // optional timing of the main sweep kernel
+};
+
+// Workspace carve-up (offsets in bytes, each 256-byte aligned).
+struct WsLayout {
+    size_t loss_part;   // float [max_parts]
+    size_t tgt_b;       // int32 [nnz_max]  sample of each positive pair
+    size_t dx_part;     // float [max_parts][B_max][d]
+    size_t total;
+};
+WsLayout ws_layout(int32_t d, int32_t B_max, int32_t nnz_max, int max_parts);
+int max_parts_for(int num_cu);
+
+// ---------------------------------------------------------------- errors
+
+void set_error(const char *fmt, ...);
+int fail(int code, const char *fmt, ...);
+int check_launch(const char *what);
+
+// ---------------------------------------------------------------- device helpers
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) {
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// fp32 -> bf16 with round-to-nearest-even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+template <int VT> struct ValueT;
+template <> struct ValueT<FFSL_F32> {
+    using T = float;
+    __device__ static __forceinline__ float load(const float *p, int64_t i) { return p[i]; }
+    __device__ static __forceinline__ void store(float *p, int64_t i, float x) { p[i] = x; }
+};
+template <> struct ValueT<FFSL_BF16> {
+    using T = uint16_t;
+    __device__ static __forceinline__ float load(const uint16_t *p, int64_t i) {
+        return bf16_bits_to_f32(p[i]);
+    }
+    __device__ static __forceinline__ void store(uint16_t *p, int64_t i, float x) {
+        p[i] = f32_to_bf16_bits(x);
+    }
+};
+
+// ---------------------------------------------------------------- launches
+
+struct AdamParams {
+    float lr, b1, b2, eps, wd;
+    float bc1, bc2;   // 1 - b1^t, 1 - b2^t (computed in double on the host)
+};
+
+enum SweepMode { SWEEP_FWD = 0, SWEEP_BWD = 1, SWEEP_FUSED = 2 };
+
+struct SweepCall {
+    const Layer *layer;
+    const void *X;
+    int32_t B;
+    const int32_t *tgt_off, *tgt_lab;
+    int32_t nnz;
+    float s;
+    int mode;
+    AdamParams adam;
+    float *loss_out;
+    float *logits_out;
+    float *dX_out;
+    uint32_t flags;
+    hipStream_t stream;
+};
+
+int launch_sweep(const SweepCall &c);
+int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
+int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
+               uint8_t *mask, int32_t *exhausted, hipStream_t st);
+int launch_validate(const Layer &ly, int32_t *bad_rows, hipStream_t st);
+
+}  // namespace ffsl

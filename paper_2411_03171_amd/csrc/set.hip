@@ -1,0 +1,251 @@
+// SET prune-and-regrow of the fixed fan-in layer (Sec. 2.1 of the paper:
+// magnitude pruning, random regrowth of as many inactive weights; the
+// hyperparameter appendix: random growth with zero initialisation), applied
+// row by row so every row keeps exactly k weights (Sec. 2.2).
+//
+// One label row per lane.  The row's k indices and weights sit in
+// registers; the n smallest (|W| bits, slot) keys are found by n passes of
+// "smallest key above the previous one" (keys are unique because the slot is
+// part of the key).  Columns the row uses are marked in a per-lane bitmap in
+// LDS laid out [word][lane], so lanes never share a bank.  Candidate columns
+// come from Philox4x64-10 (Salmon et al., SC'11) keyed by the seed and
+// counted by (row, round, block); a candidate is accepted when its bitmap
+// bit is clear, and then marked.  Accepted columns go to the pruned slots in
+// ascending slot order, which become W = +0, m = v = 0.
+#include "ffsl_internal.h"
+
+namespace ffsl {
+
+namespace {
+
+constexpr int SET_THREADS = 256;
+constexpr uint64_t SET_KEY_HI = 0x5345545F52454752ull;  // "SET_REGR"
+
+// Philox4x64-10 round structure: two 64x64->128 multiplies per round, the
+// high halves mixed with the other counter words and the round key, the key
+// advanced by the Weyl increments (golden ratio, sqrt(3)-1) between rounds.
+__device__ __forceinline__ void philox4x64_10(uint64_t &c0, uint64_t &c1, uint64_t &c2,
+                                              uint64_t &c3, uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        const uint64_t n0 = hi1 ^ c1 ^ k0;
+        const uint64_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
+}
+
+struct SetArgs {
+    int64_t L;
+    int32_t d, k, n, words;  // words = ceil(d/32) bitmap words per row
+    void *W;
+    int32_t *I;
+    float *m, *v;
+    uint8_t *mask;
+    int32_t *exhausted;
+    uint64_t seed, round;
+    int64_t cap;
+};
+
+template <int KM, int VT>
+__global__ void __launch_bounds__(SET_THREADS) k_set(const SetArgs a) {
+    extern __shared__ uint32_t bitmap[];  // [words][SET_THREADS]
+    const int tid = threadIdx.x;
+    const int64_t l = (int64_t)blockIdx.x * SET_THREADS + tid;
+    if (l >= a.L) return;  // no block-level synchronisation below
+    const int k = a.k, d = a.d, n = a.n;
+
+    int idx[KM];
+    uint32_t key[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+            idx[j] = a.I[l * k + j];
+            if constexpr (VT == FFSL_BF16)
+                key[j] = static_cast<const uint16_t *>(a.W)[l * k + j] & 0x7fffu;
+            else
+                key[j] = __float_as_uint(static_cast<const float *>(a.W)[l * k + j]) & 0x7fffffffu;
+        }
+    }
+
+    // n smallest (key, slot): pass s finds the smallest pair strictly above
+    // the pair found by pass s-1.
+    uint32_t pk = 0;
+    int pj = -1;
+    uint64_t pruned_lo = 0, pruned_hi = 0;  // slot bitmask, KM <= 128
+    for (int s = 0; s < n; ++s) {
+        uint32_t bk = 0xffffffffu;
+        int bj = KM;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+            if (j < k) {
+                const bool above = key[j] > pk || (key[j] == pk && j > pj);
+                const bool better = key[j] < bk || (key[j] == bk && j < bj);
+                if (above && better) {
+                    bk = key[j];
+                    bj = j;
+                }
+            }
+        }
+        pk = bk;
+        pj = bj;
+        if (bj < 64) pruned_lo |= 1ull << bj;
+        else pruned_hi |= 1ull << (bj - 64);
+    }
+
+    // bitmap of columns held before pruning
+    for (int q = 0; q < a.words; ++q) bitmap[q * SET_THREADS + tid] = 0u;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+            const int c = min(max(idx[j], 0), d - 1);
+            bitmap[(c >> 5) * SET_THREADS + tid] |= 1u << (c & 31);
+        }
+    }
+
+    // draws; accepted columns are written at the next pruned slot directly,
+    // so first check that the row can be completed
+    int32_t acc[KM];
+    int got = 0;
+    uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
+    for (int64_t att = 0; att < a.cap && got < n; ++att) {
+        const int wsel = (int)(att & 3);
+        if (wsel == 0) {
+            w0 = (uint64_t)l;
+            w1 = a.round;
+            w2 = (uint64_t)(att >> 2);
+            w3 = 0;
+            philox4x64_10(w0, w1, w2, w3, a.seed, SET_KEY_HI);
+        }
+        const uint64_t word = wsel == 0 ? w0 : wsel == 1 ? w1 : wsel == 2 ? w2 : w3;
+        const int c = (int)__umul64hi(word, (uint64_t)d);
+        uint32_t &bw = bitmap[(c >> 5) * SET_THREADS + tid];
+        const uint32_t bit = 1u << (c & 31);
+        if (!(bw & bit)) {
+            bw |= bit;
+#pragma unroll
+            for (int q = 0; q < KM; ++q)
+                if (q == got) acc[q] = c;
+            ++got;
+        }
+    }
+    if (got < n) {
+        if (a.exhausted) atomicAdd(a.exhausted, 1);
+        if (a.mask)
+            for (int j = 0; j < k; ++j) a.mask[l * k + j] = 0;
+        return;
+    }
+
+    int q = 0;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+            const bool pr = j < 64 ? ((pruned_lo >> j) & 1ull) : ((pruned_hi >> (j - 64)) & 1ull);
+            if (pr) {
+                int32_t c = 0;
+#pragma unroll
+                for (int r = 0; r < KM; ++r)
+                    if (r == q) c = acc[r];
+                ++q;
+                const int64_t o = l * k + j;
+                a.I[o] = c;
+                if constexpr (VT == FFSL_BF16)
+                    static_cast<uint16_t *>(a.W)[o] = 0;
+                else
+                    static_cast<float *>(a.W)[o] = 0.f;
+                a.m[o] = 0.f;
+                a.v[o] = 0.f;
+            }
+            if (a.mask) a.mask[l * k + j] = pr ? 1 : 0;
+        }
+    }
+}
+
+template <int KM>
+__global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, int k, int d, int32_t *bad) {
+    const int64_t l = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (l >= L) return;
+    int idx[KM];
+    bool ok = true;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+            idx[j] = I[l * k + j];
+            ok = ok && idx[j] >= 0 && idx[j] < d;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+#pragma unroll
+        for (int q = j + 1; q < KM; ++q)
+            if (q < k && idx[j] == idx[q]) ok = false;
+    if (!ok) atomicAdd(bad, 1);
+}
+
+template <int KM, int VT>
+int set_launch_km(const SetArgs &a, hipStream_t st) {
+    const size_t shm = (size_t)a.words * SET_THREADS * sizeof(uint32_t);
+    auto kern = k_set<KM, VT>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    const int64_t blocks = (a.L + SET_THREADS - 1) / SET_THREADS;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(SET_THREADS), shm, st, a);
+    return check_launch("set_update");
+}
+
+template <int VT>
+int set_launch_vt(const SetArgs &a, hipStream_t st) {
+    if (a.k <= 8) return set_launch_km<8, VT>(a, st);
+    if (a.k <= 16) return set_launch_km<16, VT>(a, st);
+    if (a.k <= 32) return set_launch_km<32, VT>(a, st);
+    if (a.k <= 64) return set_launch_km<64, VT>(a, st);
+    return set_launch_km<128, VT>(a, st);
+}
+
+}  // namespace
+
+int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_t *mask,
+               int32_t *exhausted, hipStream_t st) {
+    SetArgs a{};
+    a.L = ly.L;
+    a.d = ly.d;
+    a.k = ly.k;
+    a.n = n;
+    a.words = (ly.d + 31) / 32;
+    a.W = ly.W;
+    a.I = ly.I;
+    a.m = ly.m;
+    a.v = ly.v;
+    a.mask = mask;
+    a.exhausted = exhausted;
+    a.seed = seed;
+    a.round = round;
+    a.cap = 64 * (int64_t)ly.k + 4096;
+    if ((size_t)a.words * SET_THREADS * 4 > 160 * 1024)
+        return fail(FFSL_EUNSUPPORTED, "input width d=%d too large for the SET bitmap", ly.d);
+    return ly.vt == FFSL_BF16 ? set_launch_vt<FFSL_BF16>(a, st) : set_launch_vt<FFSL_F32>(a, st);
+}
+
+int launch_validate(const Layer &ly, int32_t *bad, hipStream_t st) {
+    const int64_t blocks = (ly.L + 255) / 256;
+    if (ly.k <= 16)
+        hipLaunchKernelGGL(k_validate<16>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+    else if (ly.k <= 32)
+        hipLaunchKernelGGL(k_validate<32>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+    else if (ly.k <= 64)
+        hipLaunchKernelGGL(k_validate<64>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+    else
+        hipLaunchKernelGGL(k_validate<128>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+    return check_launch("validate_indices");
+}
+
+}  // namespace ffsl

@@ -1,0 +1,427 @@
+// Sweep kernels of the fixed fan-in layer: gathered forward, fused BCE,
+// both backward products and (fused mode) Adam, in one pass over the
+// [L,k] arrays (Sec. 2.2 of the paper: ELLPACK rows of exactly k weights).
+//
+// Mapping (general path):
+//   - a persistent grid of workgroups, 256 threads each; a workgroup walks
+//     chunks of 256 consecutive label rows, one row per thread, and keeps
+//     the row's k weights, indices and (backward) gradient in registers;
+//   - the batch is cut into tiles of Bt samples; a tile of X is staged in LDS
+//     as fp32 [Bt][d] so every gather X[b, I[l,j]] is an LDS read;
+//   - dX contributions of a tile are accumulated in an LDS fp32 [Bt][d]
+//     array with LDS float atomics and flushed, at a tile switch and at the
+//     end, into a per-workgroup partial; a separate kernel sums the partials
+//     in workgroup order.  Tile order alternates between consecutive chunks
+//     so a chunk starts on the tile the previous one ended with.
+//   - the loss is a per-thread sum reduced per workgroup in a fixed tree and
+//     then over workgroups in order.
+#include "ffsl_internal.h"
+
+namespace ffsl {
+
+namespace {
+
+constexpr int SW_THREADS = 256;
+constexpr int SW_MAXT = 1024;   // max batch tiles (B_max / Bt)
+constexpr int YM_WORDS = 2;     // positives bitmask words per row (Bt <= 64)
+constexpr int SW_MAX_BT = 64;
+
+struct SweepArgs {
+    int64_t L;
+    int32_t d, k, B, Bt, T, nnz;
+    int64_t nchunks;
+    const void *X;
+    void *W;
+    const int32_t *I;
+    float *bias, *m, *v, *bm, *bv, *dW, *dbias;
+    const int32_t *tgt_b, *tgt_lab;
+    float s;
+    AdamParams adam;
+    float *logits;
+    float *loss_part;
+    float *dx_part;
+    int want_loss;
+};
+
+template <int KM>
+__device__ __forceinline__ void load_row_idx(const int32_t *I, int64_t l, int k, int d, int (&idx)[KM]) {
+    if (k == KM && (KM % 4) == 0) {
+        const int4 *p = reinterpret_cast<const int4 *>(I + l * KM);
+#pragma unroll
+        for (int q = 0; q < KM / 4; ++q) {
+            int4 t = p[q];
+            idx[4 * q + 0] = t.x;
+            idx[4 * q + 1] = t.y;
+            idx[4 * q + 2] = t.z;
+            idx[4 * q + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < KM; ++j) idx[j] = (j < k) ? I[l * k + j] : 0;
+    }
+    // Clamp so that a malformed index can never address outside the LDS tile.
+#pragma unroll
+    for (int j = 0; j < KM; ++j) idx[j] = min(max(idx[j], 0), d - 1);
+}
+
+template <int KM, int VT>
+__device__ __forceinline__ void load_row_w(const void *Wv, int64_t l, int k, float (&w)[KM]) {
+    if constexpr (VT == FFSL_BF16) {
+        const uint16_t *W = static_cast<const uint16_t *>(Wv);
+        if (k == KM && (KM % 8) == 0) {
+            const uint4 *p = reinterpret_cast<const uint4 *>(W + l * KM);
+#pragma unroll
+            for (int q = 0; q < KM / 8; ++q) {
+                uint4 t = p[q];
+                uint32_t u[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    w[8 * q + 2 * h + 0] = __uint_as_float(u[h] << 16);
+                    w[8 * q + 2 * h + 1] = __uint_as_float(u[h] & 0xffff0000u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < KM; ++j) w[j] = (j < k) ? bf16_bits_to_f32(W[l * k + j]) : 0.f;
+        }
+    } else {
+        const float *W = static_cast<const float *>(Wv);
+        if (k == KM && (KM % 4) == 0) {
+            const float4 *p = reinterpret_cast<const float4 *>(W + l * KM);
+#pragma unroll
+            for (int q = 0; q < KM / 4; ++q) {
+                float4 t = p[q];
+                w[4 * q + 0] = t.x;
+                w[4 * q + 1] = t.y;
+                w[4 * q + 2] = t.z;
+                w[4 * q + 3] = t.w;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < KM; ++j) w[j] = (j < k) ? W[l * k + j] : 0.f;
+        }
+    }
+}
+
+__device__ __forceinline__ float adam_update(float p, float g, float &mm, float &vv,
+                                             const AdamParams &ap, float decay) {
+    p *= decay;
+    mm = ap.b1 * mm + (1.f - ap.b1) * g;
+    vv = ap.b2 * vv + (1.f - ap.b2) * g * g;
+    const float mhat = mm / ap.bc1;
+    const float vhat = vv / ap.bc2;
+    return p - ap.lr * mhat / (sqrtf(vhat) + ap.eps);
+}
+
+template <int KM, int VT, int MODE>
+__global__ void __launch_bounds__(SW_THREADS) k_sweep(const SweepArgs a) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    float *Xs = reinterpret_cast<float *>(smem_raw);
+    float *dXs = Xs + (size_t)a.Bt * a.d;
+    uint32_t *ym = reinterpret_cast<uint32_t *>(dXs + (MODE != SWEEP_FWD ? (size_t)a.Bt * a.d : 0));
+    __shared__ float red[SW_THREADS];
+    __shared__ uint8_t tflushed[SW_MAXT];
+
+    using VTy = typename ValueT<VT>::T;
+    const VTy *X = static_cast<const VTy *>(a.X);
+    const int tid = threadIdx.x;
+    const int d = a.d, k = a.k;
+    float loss_acc = 0.f;
+    int staged = -1;
+
+    if (MODE != SWEEP_FWD) {
+        for (int t = tid; t < SW_MAXT; t += SW_THREADS) tflushed[t] = 0;
+        for (int e = tid; e < a.Bt * d; e += SW_THREADS) dXs[e] = 0.f;
+    }
+
+    // dX partial of this workgroup: [B][d]
+    float *P = (MODE != SWEEP_FWD) ? a.dx_part + (size_t)blockIdx.x * a.B * d : nullptr;
+    const float decay = 1.f - a.adam.lr * a.adam.wd;
+
+    int ci = 0;
+    for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += gridDim.x, ++ci) {
+        const int64_t l0 = chunk * SW_THREADS;
+        const int64_t l = l0 + tid;
+        const bool valid = l < a.L;
+
+        int idx[KM];
+        float w[KM];
+        float dw[KM];
+        float bl = 0.f, db = 0.f;
+        if (valid) {
+            load_row_idx<KM>(a.I, l, k, d, idx);
+            load_row_w<KM, VT>(a.W, l, k, w);
+            if (a.bias) bl = a.bias[l];
+        } else {
+#pragma unroll
+            for (int j = 0; j < KM; ++j) {
+                idx[j] = 0;
+                w[j] = 0.f;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < KM; ++j) dw[j] = 0.f;
+
+        for (int tt = 0; tt < a.T; ++tt) {
+            const int t = (ci & 1) ? (a.T - 1 - tt) : tt;
+            const int b0 = t * a.Bt;
+            const int bn = min(a.Bt, a.B - b0);
+            __syncthreads();
+            if (t != staged) {
+                if (MODE != SWEEP_FWD && staged >= 0) {
+                    const int sb0 = staged * a.Bt;
+                    const int sbn = min(a.Bt, a.B - sb0);
+                    const bool first = tflushed[staged] == 0;
+                    for (int e = tid; e < sbn * d; e += SW_THREADS) {
+                        const float val = dXs[e];
+                        const size_t o = (size_t)sb0 * d + e;
+                        P[o] = first ? val : P[o] + val;
+                        dXs[e] = 0.f;
+                    }
+                    __syncthreads();
+                    if (tid == 0) tflushed[staged] = 1;
+                }
+                for (int e = tid; e < bn * d; e += SW_THREADS)
+                    Xs[e] = ValueT<VT>::load(X, (int64_t)b0 * d + e);
+                staged = t;
+            }
+            for (int e = tid; e < SW_THREADS * YM_WORDS; e += SW_THREADS) ym[e] = 0u;
+            __syncthreads();
+            for (int e = tid; e < a.nnz; e += SW_THREADS) {
+                const int32_t lab = a.tgt_lab[e];
+                const int32_t b = a.tgt_b[e];
+                if (lab >= l0 && lab < l0 + SW_THREADS && b >= b0 && b < b0 + bn) {
+                    const int bb = b - b0;
+                    atomicOr(&ym[(lab - l0) * YM_WORDS + (bb >> 5)], 1u << (bb & 31));
+                }
+            }
+            __syncthreads();
+            if (valid) {
+                for (int bb = 0; bb < bn; ++bb) {
+                    const float *xr = Xs + (size_t)bb * d;
+                    float xg[KM];
+                    float z = bl;
+#pragma unroll
+                    for (int j = 0; j < KM; ++j) {
+                        if (j < k) {
+                            xg[j] = xr[idx[j]];
+                            z = fmaf(w[j], xg[j], z);
+                        } else {
+                            xg[j] = 0.f;
+                        }
+                    }
+                    const float y = ((ym[tid * YM_WORDS + (bb >> 5)] >> (bb & 31)) & 1u) ? 1.f : 0.f;
+                    const float e = expf(-fabsf(z));
+                    if (MODE != SWEEP_BWD || a.want_loss)
+                        loss_acc += fmaxf(z, 0.f) - z * y + log1pf(e);
+                    if (MODE == SWEEP_FWD && a.logits) a.logits[(int64_t)(b0 + bb) * a.L + l] = z;
+                    if (MODE != SWEEP_FWD) {
+                        const float r = 1.f / (1.f + e);
+                        const float sig = z >= 0.f ? r : e * r;
+                        const float g = a.s * (sig - y);
+                        db += g;
+                        float *dxr = dXs + (size_t)bb * d;
+#pragma unroll
+                        for (int j = 0; j < KM; ++j) {
+                            if (j < k) {
+                                dw[j] = fmaf(g, xg[j], dw[j]);
+                                atomicAdd(&dxr[idx[j]], g * w[j]);
+                            }
+                        }
+                    }
+                }
+            }
+        }
+
+        if (valid && MODE == SWEEP_BWD) {
+#pragma unroll
+            for (int j = 0; j < KM; ++j)
+                if (j < k) a.dW[l * k + j] = dw[j];
+            if (a.dbias) a.dbias[l] = db;
+        }
+        if (valid && MODE == SWEEP_FUSED) {
+            VTy *W = static_cast<VTy *>(a.W);
+#pragma unroll
+            for (int j = 0; j < KM; ++j) {
+                if (j < k) {
+                    const int64_t o = l * k + j;
+                    float mm = a.m[o], vv = a.v[o];
+                    const float p = adam_update(w[j], dw[j], mm, vv, a.adam, decay);
+                    a.m[o] = mm;
+                    a.v[o] = vv;
+                    ValueT<VT>::store(W, o, p);
+                }
+            }
+            if (a.bias) {
+                float mm = a.bm[l], vv = a.bv[l];
+                a.bias[l] = adam_update(bl, db, mm, vv, a.adam, decay);
+                a.bm[l] = mm;
+                a.bv[l] = vv;
+            }
+        }
+    }
+
+    __syncthreads();
+    if (MODE != SWEEP_FWD && staged >= 0) {
+        const int sb0 = staged * a.Bt;
+        const int sbn = min(a.Bt, a.B - sb0);
+        const bool first = tflushed[staged] == 0;
+        for (int e = tid; e < sbn * d; e += SW_THREADS) {
+            const size_t o = (size_t)sb0 * d + e;
+            P[o] = first ? dXs[e] : P[o] + dXs[e];
+        }
+    }
+    red[tid] = loss_acc;
+    __syncthreads();
+    for (int s = SW_THREADS / 2; s > 0; s >>= 1) {
+        if (tid < s) red[tid] += red[tid + s];
+        __syncthreads();
+    }
+    if (tid == 0) a.loss_part[blockIdx.x] = red[0];
+}
+
+// sample index of every positive pair: tgt_b[e] = b for e in [off[b], off[b+1])
+__global__ void k_targets_prep(const int32_t *off, int32_t B, int32_t nnz, int32_t *tgt_b) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int e0 = max(0, min(off[b], nnz));
+    const int e1 = max(e0, min(off[b + 1], nnz));
+    for (int e = e0; e < e1; ++e) tgt_b[e] = b;
+}
+
+// dX[e] (+)= sum over workgroup partials in workgroup order
+__global__ void k_dx_reduce(const float *part, int nparts, int64_t n, float *out, int accum) {
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        float s = 0.f;
+        for (int p = 0; p < nparts; ++p) s += part[(size_t)p * n + e];
+        out[e] = accum ? out[e] + s : s;
+    }
+}
+
+// loss (+)= s * sum of workgroup partials, fixed order
+__global__ void k_loss_reduce(const float *part, int nparts, float s, float *out, int accum) {
+    __shared__ float red[256];
+    float acc = 0.f;
+    for (int p = threadIdx.x; p < nparts; p += 256) acc += part[p];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[0] = accum ? out[0] + s * red[0] : s * red[0];
+}
+
+template <int KM, int VT, int MODE>
+int launch_mode(const SweepArgs &a, size_t shm, int grid, hipStream_t st) {
+    auto kern = k_sweep<KM, VT, MODE>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(SW_THREADS), shm, st, a);
+    return check_launch("sweep");
+}
+
+template <int KM, int VT>
+int launch_km(int mode, const SweepArgs &a, size_t shm, int grid, hipStream_t st) {
+    switch (mode) {
+        case SWEEP_FWD: return launch_mode<KM, VT, SWEEP_FWD>(a, shm, grid, st);
+        case SWEEP_BWD: return launch_mode<KM, VT, SWEEP_BWD>(a, shm, grid, st);
+        default: return launch_mode<KM, VT, SWEEP_FUSED>(a, shm, grid, st);
+    }
+}
+
+template <int VT>
+int launch_vt(int mode, const SweepArgs &a, size_t shm, int grid, hipStream_t st) {
+    if (a.k <= 8) return launch_km<8, VT>(mode, a, shm, grid, st);
+    if (a.k <= 16) return launch_km<16, VT>(mode, a, shm, grid, st);
+    if (a.k <= 32) return launch_km<32, VT>(mode, a, shm, grid, st);
+    if (a.k <= 64) return launch_km<64, VT>(mode, a, shm, grid, st);
+    return launch_km<128, VT>(mode, a, shm, grid, st);
+}
+
+}  // namespace
+
+constexpr size_t LDS_BUDGET = 160 * 1024 - 4096;  // minus static arrays
+
+int launch_sweep(const SweepCall &c) {
+    const Layer &ly = *c.layer;
+    const int B = c.B, d = ly.d;
+    const size_t per_b = (size_t)d * sizeof(float) * (c.mode == SWEEP_FWD ? 1 : 2);
+    const size_t ym_bytes = SW_THREADS * YM_WORDS * sizeof(uint32_t);
+    int Bt = (int)std::min<size_t>((LDS_BUDGET - ym_bytes) / per_b, (size_t)SW_MAX_BT);
+    Bt = std::min(Bt, B);
+    if (Bt < 1) return fail(FFSL_EUNSUPPORTED, "input width d=%d too large for the LDS tile", d);
+    const int T = (B + Bt - 1) / Bt;
+    if (T > SW_MAXT) return fail(FFSL_EUNSUPPORTED, "too many batch tiles (%d)", T);
+    const size_t shm = (size_t)Bt * per_b + ym_bytes;
+
+    const WsLayout wl = ws_layout(d, ly.B_max, ly.nnz_max, ly.max_parts);
+    SweepArgs a{};
+    a.L = ly.L;
+    a.d = d;
+    a.k = ly.k;
+    a.B = B;
+    a.Bt = Bt;
+    a.T = T;
+    a.nnz = c.nnz;
+    a.nchunks = (ly.L + SW_THREADS - 1) / SW_THREADS;
+    a.X = c.X;
+    a.W = ly.W;
+    a.I = ly.I;
+    a.bias = ly.bias;
+    a.m = ly.m;
+    a.v = ly.v;
+    a.bm = ly.bm;
+    a.bv = ly.bv;
+    a.dW = ly.dW;
+    a.dbias = ly.dbias;
+    a.tgt_b = reinterpret_cast<const int32_t *>(ly.ws + wl.tgt_b);
+    a.tgt_lab = c.tgt_lab;
+    a.s = c.s;
+    a.adam = c.adam;
+    a.logits = c.logits_out;
+    a.loss_part = reinterpret_cast<float *>(ly.ws + wl.loss_part);
+    a.dx_part = reinterpret_cast<float *>(ly.ws + wl.dx_part);
+    a.want_loss = c.loss_out != nullptr;
+
+    const int grid = (int)std::min<int64_t>(a.nchunks, ly.max_parts);
+
+    if (c.nnz > 0) {
+        hipLaunchKernelGGL(k_targets_prep, dim3((B + 255) / 256), dim3(256), 0, c.stream, c.tgt_off, B,
+                           c.nnz, const_cast<int32_t *>(a.tgt_b));
+        int rc = check_launch("targets_prep");
+        if (rc) return rc;
+    }
+
+    if (ly.ev_start) {
+        hipError_t e = hipEventRecord(ly.ev_start, c.stream);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    int rc = (ly.vt == FFSL_BF16) ? launch_vt<FFSL_BF16>(c.mode, a, shm, grid, c.stream)
+                                  : launch_vt<FFSL_F32>(c.mode, a, shm, grid, c.stream);
+    if (rc) return rc;
+    if (ly.ev_stop) {
+        hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+
+    if (c.loss_out) {
+        hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, a.loss_part, grid, c.s,
+                           c.loss_out, (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0);
+        rc = check_launch("loss_reduce");
+        if (rc) return rc;
+    }
+    if (c.mode != SWEEP_FWD && c.dX_out) {
+        const int64_t n = (int64_t)B * d;
+        const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
+        hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, a.dx_part, grid, n,
+                           c.dX_out, (c.flags & FFSL_ACCUM_DX) ? 1 : 0);
+        rc = check_launch("dx_reduce");
+        if (rc) return rc;
+    }
+    return FFSL_OK;
+}
+
+}  // namespace ffsl

@@ -82,12 +82,18 @@ def scaled(w: Workload, L: Optional[int] = None, B: Optional[int] = None,
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (ties to even); returns uint16 bit patterns."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    nan = np.isnan(np.asarray(x, dtype=np.float32))
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
-    r[nan] = 0x7FC0
-    return r
+    x32 = np.ascontiguousarray(x, dtype=np.float32)
+    u = x32.view(np.uint32)
+    # for every non-NaN pattern u + 0x8000 stays below 2^32, so uint32 is exact
+    r = (u >> 16) & np.uint32(1)
+    r += u
+    r += np.uint32(0x7FFF)
+    r >>= np.uint32(16)
+    out = r.astype(np.uint16)
+    nan = np.isnan(x32)
+    if nan.any():
+        out[nan] = 0x7FC0
+    return out
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -124,10 +130,17 @@ def gen_x(rng: np.random.Generator, B: int, d: int, norm: str, value: str) -> np
     return x32 if value == "f32" else f32_to_bf16_bits(x32)
 
 
-def gen_w(rng: np.random.Generator, L: int, k: int, value: str) -> np.ndarray:
-    a = 1.0 / np.sqrt(k)
-    w32 = rng.uniform(-a, a, size=(L, k)).astype(np.float32)
-    return w32 if value == "f32" else f32_to_bf16_bits(w32)
+def gen_w(rng: np.random.Generator, L: int, k: int, value: str, chunk: int = 1 << 18) -> np.ndarray:
+    """U(-1/sqrt(k), 1/sqrt(k)) weights, drawn in float32 chunk by chunk."""
+    a = np.float32(1.0 / np.sqrt(k))
+    out = np.empty((L, k), dtype=np.float32 if value == "f32" else np.uint16)
+    for s in range(0, L, chunk):
+        e = min(L, s + chunk)
+        w32 = rng.random((e - s, k), dtype=np.float32)
+        w32 *= 2 * a
+        w32 -= a
+        out[s:e] = w32 if value == "f32" else f32_to_bf16_bits(w32)
+    return out
 
 
 def gen_indices(rng: np.random.Generator, L: int, k: int, d: int, chunk: int = 1 << 20) -> np.ndarray:

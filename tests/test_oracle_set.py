@@ -48,7 +48,7 @@ def absbits(Wbits):
     return (Wbits & 0x7FFFFFFF).astype(np.int64)
 
 
-def python_set(Wbits, I, d, frac, seed, set_round, allow=False):
+def python_set(Wbits, I, d, frac, seed, set_round, allow=False, row0=0):
     """The SET contract re-derived in plain Python on numpy's Philox."""
     Wb, I = Wbits.copy(), I.copy()
     L, k = I.shape
@@ -68,7 +68,7 @@ def python_set(Wbits, I, d, frac, seed, set_round, allow=False):
             if len(acc) == n:
                 break
             if a % 4 == 0:
-                block = numpy_philox_block((l, set_round, a // 4, 0), (seed, SET_KEY_HI))
+                block = numpy_philox_block((row0 + l, set_round, a // 4, 0), (seed, SET_KEY_HI))
             c = (int(block[a % 4]) * d) >> 64
             if c not in pre and c not in acc:
                 acc.append(c)
@@ -220,3 +220,14 @@ def test_set_regrowth_is_uniform(oracle):
     # 55 degrees of freedom: the 0.999 quantile is about 93
     assert chi2 < 93, chi2
     assert counts.min() > 0
+
+
+def test_set_row_block_equals_whole_layer(oracle):
+    W, I, m, v = make_state(6, 400, 16, 96)
+    whole = oracle.set_update(W, I, m, v, 96, 0.25, seed=11, set_round=2)
+    blk = oracle.set_update(W[150:260], I[150:260], m[150:260], v[150:260], 96, 0.25, seed=11,
+                            set_round=2, row0=150)
+    assert np.array_equal(whole[1][150:260], blk[1])
+    assert np.array_equal(whole[4][150:260], blk[4])
+    _, Ir, _ = python_set(W[150:260], I[150:260], 96, 0.25, 11, 2, row0=150)
+    assert np.array_equal(Ir, blk[1])
