@@ -155,6 +155,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--set-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="run one plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -199,6 +201,19 @@ def main():
     torch.cuda.synchronize()
     print("[bench] state resident: %.1f MB" % (torch.cuda.memory_allocated() / 1e6),
           file=sys.stderr, flush=True)
+
+    if args.copy_probe_mb:
+        # a plain copy of known size: under rocprofv3 --pmc its FETCH_SIZE and
+        # WRITE_SIZE give the counters' scale for the sweep kernel's traffic
+        nb = args.copy_probe_mb << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        print("[bench] copy probe: %d MiB read + %d MiB written" % (args.copy_probe_mb,
+              args.copy_probe_mb), file=sys.stderr, flush=True)
 
     ev = HipEvents()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)

@@ -3,23 +3,28 @@
 // hyperparameter appendix: random growth with zero initialisation), applied
 // row by row so every row keeps exactly k weights (Sec. 2.2).
 //
-// One label row per lane.  The row's k indices and weights sit in
-// registers; the n smallest (|W| bits, slot) keys are found by n passes of
-// "smallest key above the previous one" (keys are unique because the slot is
-// part of the key).  Columns the row uses are marked in a per-lane bitmap in
-// LDS laid out [word][lane], so lanes never share a bank.  Candidate columns
-// come from Philox4x64-10 (Salmon et al., SC'11) keyed by the seed and
-// counted by (row, round, block); a candidate is accepted when its bitmap
-// bit is clear, and then marked.  Accepted columns go to the pruned slots in
-// ascending slot order, which become W = +0, m = v = 0.
+// A workgroup owns R consecutive label rows, one row per lane.  It first
+// copies the R rows of I and W into LDS with coalesced 16-byte loads (the
+// rows are contiguous in HBM), padded by one word per row so that lane t
+// reading its own row hits bank t.  Each lane then:
+//   - builds its keys (|W| bits, slot) and selects the n smallest with n
+//     passes of "smallest key above the previous one" (keys are unique
+//     because the slot is part of the key);
+//   - marks the row's columns in a private bitmap in LDS laid out
+//     [word][lane], so lanes never share a bank;
+//   - draws candidates from Philox4x64-10 (Salmon et al., SC'11) keyed by the
+//     seed and counted by (row, round, block), accepting a candidate whose
+//     bitmap bit is clear and then marking it;
+//   - writes the accepted columns to the pruned slots in ascending slot
+//     order, with W = +0 and m = v = 0; all other slots are left untouched.
 #include "ffsl_internal.h"
 
 namespace ffsl {
 
 namespace {
 
-constexpr int SET_THREADS = 256;
 constexpr uint64_t SET_KEY_HI = 0x5345545F52454752ull;  // "SET_REGR"
+constexpr int SET_MAX_ROWS = 256;
 
 // Philox4x64-10 round structure: two 64x64->128 multiplies per round, the
 // high halves mixed with the other counter words and the round key, the key
@@ -46,6 +51,7 @@ __device__ __forceinline__ void philox4x64_10(uint64_t &c0, uint64_t &c1, uint64
 struct SetArgs {
     int64_t L;
     int32_t d, k, n, words;  // words = ceil(d/32) bitmap words per row
+    int32_t R;               // rows (= threads) per workgroup
     void *W;
     int32_t *I;
     float *m, *v;
@@ -55,24 +61,92 @@ struct SetArgs {
     int64_t cap;
 };
 
+// LDS layout (32-bit words): bitmap [words][R], Itile [R][k+1], Wtile [R][kw+1]
+// where kw = k (fp32 W) or ceil(k/2) (bf16 W, two per word).
+template <int VT>
+__host__ __device__ inline int w_words(int k) {
+    return VT == FFSL_BF16 ? (k + 1) / 2 : k;
+}
+
 template <int KM, int VT>
-__global__ void __launch_bounds__(SET_THREADS) k_set(const SetArgs a) {
-    extern __shared__ uint32_t bitmap[];  // [words][SET_THREADS]
-    const int tid = threadIdx.x;
-    const int64_t l = (int64_t)blockIdx.x * SET_THREADS + tid;
-    if (l >= a.L) return;  // no block-level synchronisation below
+__global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
+    extern __shared__ uint32_t lds[];
+    const int R = a.R;
     const int k = a.k, d = a.d, n = a.n;
+    const int kw = w_words<VT>(k);
+    uint32_t *bitmap = lds;
+    uint32_t *Itile = bitmap + (size_t)a.words * R;
+    uint32_t *Wtile = Itile + (size_t)R * (k + 1);
+
+    const int tid = threadIdx.x;
+    const int64_t l0 = (int64_t)blockIdx.x * R;
+    const int rows = (int)min<int64_t>(R, a.L - l0);
+
+    // stage I and W rows (contiguous in HBM) into padded LDS rows
+    {
+        const uint32_t *Ig = reinterpret_cast<const uint32_t *>(a.I) + l0 * k;
+        const int nI = rows * k;
+        if ((k & 3) == 0) {
+            const uint4 *Ig4 = reinterpret_cast<const uint4 *>(Ig);
+            for (int e4 = tid; e4 < nI / 4; e4 += R) {
+                const uint4 q = Ig4[e4];
+                const int e = 4 * e4, r = e / k, j = e - r * k;
+                uint32_t *dst = Itile + r * (k + 1) + j;
+                dst[0] = q.x;
+                dst[1] = q.y;
+                dst[2] = q.z;
+                dst[3] = q.w;
+            }
+        } else {
+            for (int e = tid; e < nI; e += R) {
+                const int r = e / k, j = e - r * k;
+                Itile[r * (k + 1) + j] = Ig[e];
+            }
+        }
+        if constexpr (VT == FFSL_BF16) {
+            const uint16_t *Wg = static_cast<const uint16_t *>(a.W) + l0 * k;
+            uint16_t *Wt = reinterpret_cast<uint16_t *>(Wtile);
+            if ((k & 7) == 0) {
+                const uint4 *Wg4 = reinterpret_cast<const uint4 *>(Wg);
+                for (int e8 = tid; e8 < nI / 8; e8 += R) {
+                    const uint4 q = Wg4[e8];
+                    const int e = 8 * e8, r = e / k, j = e - r * k;
+                    uint32_t *dst = Wtile + r * (kw + 1) + j / 2;
+                    dst[0] = q.x;
+                    dst[1] = q.y;
+                    dst[2] = q.z;
+                    dst[3] = q.w;
+                }
+            } else {
+                for (int e = tid; e < nI; e += R) {
+                    const int r = e / k, j = e - r * k;
+                    Wt[2 * (r * (kw + 1)) + j] = Wg[e];
+                }
+            }
+        } else {
+            const uint32_t *Wg = static_cast<const uint32_t *>(a.W) + l0 * k;
+            for (int e = tid; e < nI; e += R) {
+                const int r = e / k, j = e - r * k;
+                Wtile[r * (kw + 1) + j] = Wg[e];
+            }
+        }
+    }
+    __syncthreads();
+    if (tid >= rows) return;  // no block-level synchronisation below
+    const int64_t l = l0 + tid;
 
     int idx[KM];
     uint32_t key[KM];
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
         if (j < k) {
-            idx[j] = a.I[l * k + j];
-            if constexpr (VT == FFSL_BF16)
-                key[j] = static_cast<const uint16_t *>(a.W)[l * k + j] & 0x7fffu;
-            else
-                key[j] = __float_as_uint(static_cast<const float *>(a.W)[l * k + j]) & 0x7fffffffu;
+            idx[j] = (int)Itile[tid * (k + 1) + j];
+            if constexpr (VT == FFSL_BF16) {
+                const uint32_t pair = Wtile[tid * (kw + 1) + j / 2];
+                key[j] = ((j & 1) ? (pair >> 16) : pair) & 0x7fffu;
+            } else {
+                key[j] = Wtile[tid * (kw + 1) + j] & 0x7fffffffu;
+            }
         }
     }
 
@@ -102,17 +176,16 @@ __global__ void __launch_bounds__(SET_THREADS) k_set(const SetArgs a) {
     }
 
     // bitmap of columns held before pruning
-    for (int q = 0; q < a.words; ++q) bitmap[q * SET_THREADS + tid] = 0u;
+    for (int q = 0; q < a.words; ++q) bitmap[q * R + tid] = 0u;
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
         if (j < k) {
             const int c = min(max(idx[j], 0), d - 1);
-            bitmap[(c >> 5) * SET_THREADS + tid] |= 1u << (c & 31);
+            bitmap[(c >> 5) * R + tid] |= 1u << (c & 31);
         }
     }
 
-    // draws; accepted columns are written at the next pruned slot directly,
-    // so first check that the row can be completed
+    // draws
     int32_t acc[KM];
     int got = 0;
     uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
@@ -127,7 +200,7 @@ __global__ void __launch_bounds__(SET_THREADS) k_set(const SetArgs a) {
         }
         const uint64_t word = wsel == 0 ? w0 : wsel == 1 ? w1 : wsel == 2 ? w2 : w3;
         const int c = (int)__umul64hi(word, (uint64_t)d);
-        uint32_t &bw = bitmap[(c >> 5) * SET_THREADS + tid];
+        uint32_t &bw = bitmap[(c >> 5) * R + tid];
         const uint32_t bit = 1u << (c & 31);
         if (!(bw & bit)) {
             bw |= bit;
@@ -164,7 +237,31 @@ __global__ void __launch_bounds__(SET_THREADS) k_set(const SetArgs a) {
                 a.m[o] = 0.f;
                 a.v[o] = 0.f;
             }
-            if (a.mask) a.mask[l * k + j] = pr ? 1 : 0;
+        }
+    }
+    if (a.mask) {
+        // k bytes per row, packed 4 per word when the row is word aligned
+        if ((k & 3) == 0) {
+            uint32_t *mrow = reinterpret_cast<uint32_t *>(a.mask + l * k);
+#pragma unroll
+            for (int j4 = 0; j4 < KM / 4; ++j4) {
+                if (4 * j4 < k) {
+                    uint32_t wv = 0;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const int j = 4 * j4 + h;
+                        const uint32_t pr =
+                            j < 64 ? (uint32_t)((pruned_lo >> j) & 1ull) : (uint32_t)((pruned_hi >> (j - 64)) & 1ull);
+                        wv |= pr << (8 * h);
+                    }
+                    mrow[j4] = wv;
+                }
+            }
+        } else {
+            for (int j = 0; j < k; ++j) {
+                const bool pr = j < 64 ? ((pruned_lo >> j) & 1ull) : ((pruned_hi >> (j - 64)) & 1ull);
+                a.mask[l * k + j] = pr ? 1 : 0;
+            }
         }
     }
 }
@@ -190,15 +287,25 @@ __global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, i
     if (!ok) atomicAdd(bad, 1);
 }
 
+template <int VT>
+size_t set_lds_bytes(int words, int R, int k) {
+    return sizeof(uint32_t) * ((size_t)words * R + (size_t)R * (k + 1) + (size_t)R * (w_words<VT>(k) + 1));
+}
+
 template <int KM, int VT>
-int set_launch_km(const SetArgs &a, hipStream_t st) {
-    const size_t shm = (size_t)a.words * SET_THREADS * sizeof(uint32_t);
+int set_launch_km(SetArgs a, hipStream_t st) {
+    constexpr size_t LDS_MAX = 160 * 1024;
+    int R = SET_MAX_ROWS;
+    while (R > 64 && set_lds_bytes<VT>(a.words, R, a.k) > LDS_MAX) R /= 2;
+    const size_t shm = set_lds_bytes<VT>(a.words, R, a.k);
+    if (shm > LDS_MAX) return fail(FFSL_EUNSUPPORTED, "SET tile does not fit LDS (d=%d, k=%d)", a.d, a.k);
+    a.R = R;
     auto kern = k_set<KM, VT>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
     if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
-    const int64_t blocks = (a.L + SET_THREADS - 1) / SET_THREADS;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(SET_THREADS), shm, st, a);
+    const int64_t blocks = (a.L + R - 1) / R;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(R), shm, st, a);
     return check_launch("set_update");
 }
 
@@ -230,8 +337,6 @@ int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_
     a.seed = seed;
     a.round = round;
     a.cap = 64 * (int64_t)ly.k + 4096;
-    if ((size_t)a.words * SET_THREADS * 4 > 160 * 1024)
-        return fail(FFSL_EUNSUPPORTED, "input width d=%d too large for the SET bitmap", ly.d);
     return ly.vt == FFSL_BF16 ? set_launch_vt<FFSL_BF16>(a, st) : set_launch_vt<FFSL_F32>(a, st);
 }
 
