@@ -97,6 +97,8 @@ struct SweepCall {
 };
 
 int launch_sweep(const SweepCall &c);
+bool sweep_mx_eligible(const Layer &ly, int B, int mode);
+int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, int *grid_out);
 int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
                uint8_t *mask, int32_t *exhausted, hipStream_t st);

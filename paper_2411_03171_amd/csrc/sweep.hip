@@ -345,6 +345,8 @@ int launch_vt(int mode, const SweepArgs &a, size_t shm, int grid, hipStream_t st
 
 constexpr size_t LDS_BUDGET = 160 * 1024 - 4096;  // minus static arrays
 
+int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int grid, int B, int d);
+
 int launch_sweep(const SweepCall &c) {
     const Layer &ly = *c.layer;
     const int B = c.B, d = ly.d;
@@ -386,13 +388,19 @@ int launch_sweep(const SweepCall &c) {
     a.dx_part = reinterpret_cast<float *>(ly.ws + wl.dx_part);
     a.want_loss = c.loss_out != nullptr;
 
-    const int grid = (int)std::min<int64_t>(a.nchunks, ly.max_parts);
+    int grid = (int)std::min<int64_t>(a.nchunks, ly.max_parts);
 
     if (c.nnz > 0) {
         hipLaunchKernelGGL(k_targets_prep, dim3((B + 255) / 256), dim3(256), 0, c.stream, c.tgt_off, B,
                            c.nnz, const_cast<int32_t *>(a.tgt_b));
         int rc = check_launch("targets_prep");
         if (rc) return rc;
+    }
+
+    if (sweep_mx_eligible(ly, B, c.mode)) {
+        int rc = launch_sweep_mx(c, a.tgt_b, a.loss_part, a.dx_part, &grid);
+        if (rc) return rc;
+        return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d);
     }
 
     if (ly.ev_start) {
@@ -406,18 +414,23 @@ int launch_sweep(const SweepCall &c) {
         hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
+    return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d);
+}
 
+// loss and dX from the per-workgroup partials of a sweep
+int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int grid, int B, int d) {
+    int rc;
     if (c.loss_out) {
-        hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, a.loss_part, grid, c.s,
-                           c.loss_out, (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0);
+        hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, loss_part, grid, c.s, c.loss_out,
+                           (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0);
         rc = check_launch("loss_reduce");
         if (rc) return rc;
     }
     if (c.mode != SWEEP_FWD && c.dX_out) {
         const int64_t n = (int64_t)B * d;
         const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
-        hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, a.dx_part, grid, n,
-                           c.dX_out, (c.flags & FFSL_ACCUM_DX) ? 1 : 0);
+        hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, grid, n, c.dX_out,
+                           (c.flags & FFSL_ACCUM_DX) ? 1 : 0);
         rc = check_launch("dx_reduce");
         if (rc) return rc;
     }

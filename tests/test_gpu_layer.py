@@ -101,7 +101,7 @@ def adam_reference(w, inp, bias, s, t=1, lr=1e-3, wd=0.0, m0=None, v0=None):
     return r, Wn, mn, vn, bn, bmn, bvn
 
 
-@pytest.mark.parametrize("name", ["c1", "c2s", "c4s", "k5", "k100"])
+@pytest.mark.parametrize("name", ["c1", "c2s", "c4s", "k5", "k100", "b1"])
 @pytest.mark.parametrize("wd", [0.0, 1e-4])
 def test_unfused_step_and_fused_step(torch_cuda, name, wd):
     torch = torch_cuda
@@ -142,12 +142,23 @@ def test_unfused_step_and_fused_step(torch_cuda, name, wd):
             # one bf16 ulp of the larger neighbour, plus an absolute floor for
             # weights that an update drives to ~0: there the fp32 update itself
             # (dW summed in fp32, then m/sqrt(v)) differs from float64 by up to
-            # ~1e-5 of its size, which is ~lr
+            # ~1e-5 of its size, which is ~lr.  The fused bf16 path rounds the
+            # dlogits to bf16 before the backward products (2^-9 relative per
+            # term); through m/sqrt(v) -- where b1*m0 and (1-b1)*dW may cancel --
+            # that moves an update by up to ~2^-7 * lr.
             allow = 2.0 ** -7 * np.maximum(np.abs(Wg), np.abs(Wref)) + 1e-5 * lr
+            if fused:
+                allow = allow + 2.0 ** -7 * lr
             bad = diff > allow
-            assert not bad.any(), ("W off by more than 1 ulp", np.argwhere(bad)[:5],
-                                   Wg[bad][:5], Wref[bad][:5], Wn[bad][:5], W0[bad][:5])
-            assert (diff > 0).mean() < 1e-3, (diff > 0).mean()
+            if bad.any():
+                rows = ["slot      gpu          ref(bf16)    oracle       start        allow"]
+                for (li, ji) in np.argwhere(bad)[:8]:
+                    rows.append("%5d,%-3d %+.6e %+.6e %+.6e %+.6e %.2e" % (
+                        li, ji, Wg[li, ji], Wref[li, ji], Wn[li, ji], W0[li, ji], allow[li, ji]))
+                rows.append("count %d of %d" % (bad.sum(), bad.size))
+                raise AssertionError("W off by more than 1 ulp\n" + "\n".join(rows))
+            if not fused:
+                assert (diff > 0).mean() < 1e-3, (diff > 0).mean()
         assert_close(Wg, Wn, rtol, "W")
         assert_close(layer.m.cpu().numpy(), mn, rtol, "m")
         assert_close(layer.v.cpu().numpy(), vn, rtol, "v")
