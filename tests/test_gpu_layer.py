@@ -26,6 +26,10 @@ CASES = {
     "kfull": synth.scaled(W1["c1_fp32_L4096"], L=300, d=16, k=16, B=7, name="kfull"),
     "k100": synth.scaled(W1["c4_bf16_L3M"], L=600, k=100, B=20, name="k100"),
     "b1": synth.scaled(W1["c4_bf16_L3M"], L=513, B=1, name="b1"),
+    # the fused bf16 fan-in-32 fast path at other widths (narrowest, odd tile
+    # count) with a ragged batch
+    "mx64": synth.scaled(W1["c4_bf16_L3M"], L=257, d=64, B=64, name="mx64"),
+    "mx320": synth.scaled(W1["c4_bf16_L3M"], L=1003, d=320, B=37, name="mx320"),
 }
 
 
