@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
 
 def sweep_source_hash():
     h = hashlib.sha256()
-    for name in ("sweep.hip", "ffsl_internal.h"):
+    for name in ("sweep.hip", "sweep_mx.hip", "ffsl_internal.h"):
         with open(os.path.join(ROOT, "paper_2411_03171_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -290,7 +290,7 @@ def main():
                    "positives_mean": w.mean_pos, "zipf_s": w.zipf_s},
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_sweep (fused mode)",
+            "kernel": "k_sweep_mx (fused bf16 fan-in-32 path)" if (w.value == "bf16" and w.k == 32 and w.B <= 64) else "k_sweep (fused mode)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

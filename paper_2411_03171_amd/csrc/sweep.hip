@@ -397,7 +397,8 @@ int launch_sweep(const SweepCall &c) {
         if (rc) return rc;
     }
 
-    if (sweep_mx_eligible(ly, B, c.mode)) {
+    // the fast path reads X in 16-byte rows
+    if (sweep_mx_eligible(ly, B, c.mode) && (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
         int rc = launch_sweep_mx(c, a.tgt_b, a.loss_part, a.dx_part, &grid);
         if (rc) return rc;
         return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d);

@@ -31,9 +31,14 @@
 //   6. dX: g and the old weights go to G and T, and the matrix cores add
 //      G x T^T (64 x 32 by 32 x d) into a per-workgroup dX held in AGPRs for
 //      the workgroup's whole life; it is written out once at the end.
-// The next chunk's index and weight rows are loaded into registers while the
-// current chunk computes; the matrix-core work of a chunk overlaps the VALU
-// work of the next.
+// The next chunk's index and weight rows and the optimiser state of its slots
+// are loaded into registers while the current chunk computes; the
+// matrix-core work of a chunk overlaps the VALU work of the next.  All HBM
+// accesses of the chunk loop are range-checked buffer operations: a row past
+// L reads zeros and its writes are dropped by the hardware, so the loop has no
+// data-dependent branches and the compiler can keep exact counts of
+// outstanding memory operations (a branch around a store makes it drain them
+// all).
 #include "ffsl_internal.h"
 
 namespace ffsl {
@@ -65,7 +70,39 @@ struct MxArgs {
     AdamParams adam;
     float *loss_part;
     float *dx_part;
-    int want_loss;
+    // array sizes in bytes: the range of each buffer resource, and the offset
+    // that the chunk loop uses for an access that must not happen
+    uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+};
+
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+// raw buffer resource over [p, p + nbytes): out-of-range loads read 0 and
+// out-of-range stores are dropped
+__device__ __forceinline__ Rsrc make_rsrc(const void *p, uint32_t nbytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)nbytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint32_t ld32(Rsrc r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ float ldf(Rsrc r, uint32_t off) { return __uint_as_float(ld32(r, off)); }
+__device__ __forceinline__ float2 ldf2(Rsrc r, uint32_t off) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+}
+__device__ __forceinline__ void st32(Rsrc r, uint32_t off, uint32_t x) {
+    __builtin_amdgcn_raw_buffer_store_b32(x, r, off, 0, 0);
+}
+__device__ __forceinline__ void stf(Rsrc r, uint32_t off, float x) { st32(r, off, __float_as_uint(x)); }
+__device__ __forceinline__ void stf2(Rsrc r, uint32_t off, float2 x) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = {__float_as_uint(x.x), __float_as_uint(x.y)};
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+}
+
+struct Rsrcs {
+    Rsrc X, W, I, m, v, b, bm, bv;
 };
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -100,25 +137,42 @@ __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &v
     p *= decay;
     mm = b1 * mm + (1.f - b1) * g;
     vv = b2 * vv + (1.f - b2) * g * g;
-    const float den = sqrtf(vv * inv_bc2) + eps;
-    return p - lr * (mm * inv_bc1) / den;
+    const float den = __builtin_amdgcn_sqrtf(vv * inv_bc2) + eps;
+    return p - (lr * inv_bc1) * mm * __builtin_amdgcn_rcpf(den);
 }
 
 struct Prefetch {
-    int4 iv;      // four index words of the chunk's I rows
-    uint2 wv;     // two weight words of the chunk's W rows
+    uint4 iv;                        // four index words of the chunk's I rows
+    uint2 wv;                        // two weight words of the chunk's W rows
+    float2 m[MX_ROWS], v[MX_ROWS];   // moments of slots K, K+1 of the lane's rows
+    float b[MX_ROWS], bm[MX_ROWS], bv[MX_ROWS];   // bias and its moments
 };
 
-// the next chunk's I and W words, loaded a chunk ahead of their use
-__device__ __forceinline__ void prefetch(const MxArgs &a, int64_t chunk, int tid, Prefetch &p) {
+// the chunk's rows and optimiser state, loaded a chunk ahead of their use; a
+// chunk or row past the end reads zeros
+__device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_t chunk, int tid, int lab, int u,
+                                         int K, Prefetch &p) {
     const int64_t l0 = chunk * MX_NLAB;
-    const int64_t bi = l0 * MX_K + 4 * tid;
-    p.iv = make_int4(0, 0, 0, 0);
-    if (chunk < a.nchunks && bi + 3 < a.L * MX_K) p.iv = *reinterpret_cast<const int4 *>(a.I + bi);
-    const int64_t bw = l0 * (MX_K / 2) + 2 * tid;
-    p.wv = make_uint2(0u, 0u);
-    if (chunk < a.nchunks && bw + 1 < a.L * (MX_K / 2))
-        p.wv = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint32_t *>(a.W) + bw);
+    const bool live = chunk < a.nchunks;
+    const uint32_t oi = live ? (uint32_t)(l0 * MX_K * 4) + 16u * tid : a.nb_I;
+    const auto iv = __builtin_amdgcn_raw_buffer_load_b128(R.I, oi, 0, 0);
+    p.iv = make_uint4(iv[0], iv[1], iv[2], iv[3]);
+    const uint32_t ow = live ? (uint32_t)(l0 * MX_K * 2) + 8u * tid : a.nb_W;
+    const auto wv = __builtin_amdgcn_raw_buffer_load_b64(R.W, ow, 0, 0);
+    p.wv = make_uint2(wv[0], wv[1]);
+#pragma unroll
+    for (int h = 0; h < MX_ROWS; ++h) {
+        const int64_t l = l0 + lab + 16 * h;
+        const bool ok = live && l < a.L;
+        const uint32_t om = ok ? (uint32_t)(l * MX_K + K) * 4u : a.nb_m;
+        p.m[h] = ldf2(R.m, om);
+        p.v[h] = ldf2(R.v, om);
+        const uint32_t ob = ok ? (uint32_t)l * 4u : a.nb_b;
+        p.b[h] = ldf(R.b, ob);
+        const uint32_t obm = u == 0 ? ob : a.nb_b;
+        p.bm[h] = ldf(R.bm, obm);
+        p.bv[h] = ldf(R.bv, obm);
+    }
 }
 
 // NT = column tiles of 16 per wave: d = 64 * NT (a compile-time width keeps
@@ -141,15 +195,35 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     const int K = lane_key(u);
     const bool tg_lds = a.nnz <= MX_TG_MAX;
 
+    Rsrcs R;
+    R.X = make_rsrc(a.X, a.nb_X);
+    R.W = make_rsrc(a.W, a.nb_W);
+    R.I = make_rsrc(a.I, a.nb_I);
+    R.m = make_rsrc(a.m, a.nb_m);
+    R.v = make_rsrc(a.v, a.nb_m);
+    R.b = make_rsrc(a.bias, a.nb_b);
+    R.bm = make_rsrc(a.bm, a.nb_b);
+    R.bv = make_rsrc(a.bv, a.nb_b);
+
     Prefetch cur, nxt;
-    prefetch(a, blockIdx.x, tid, cur);
+    prefetch(a, R, blockIdx.x, tid, lab, u, K, cur);
 
     // stage X transposed (b fastest) and zero past B; clear T; keep the positives
     {
+        // lane = sample, each wave takes groups of 8 columns: 16-byte row loads,
+        // conflict-free 2-byte LDS stores
         uint16_t *X16 = reinterpret_cast<uint16_t *>(Xs);
-        for (int e = tid; e < d * MX_NB; e += MX_THREADS) {
-            const int i = e >> 6, b = e & 63;
-            X16[e] = b < a.B ? a.X[(size_t)b * d + i] : (uint16_t)0;
+        const int b = lane;
+#pragma unroll 6
+        for (int gi = wave; gi < d / 8; gi += MX_THREADS / 64) {
+            const uint32_t ox = b < a.B ? (uint32_t)(b * d + 8 * gi) * 2u : a.nb_X;
+            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.X, ox, 0, 0);
+            const uint32_t w4[4] = {q[0], q[1], q[2], q[3]};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                X16[(8 * gi + 2 * j) * MX_NB + b] = (uint16_t)(w4[j] & 0xffffu);
+                X16[(8 * gi + 2 * j + 1) * MX_NB + b] = (uint16_t)(w4[j] >> 16);
+            }
         }
         for (int e = tid; e < d * MX_NLAB / 2; e += MX_THREADS) reinterpret_cast<uint32_t *>(T)[e] = 0u;
         if (tg_lds)
@@ -176,13 +250,13 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         // stage this chunk's rows (loaded during the previous chunk): indices
         // become clamped byte offsets of X columns
         {
-            const int i0 = min(max(cur.iv.x, 0), d - 1), i1 = min(max(cur.iv.y, 0), d - 1);
-            const int i2 = min(max(cur.iv.z, 0), d - 1), i3 = min(max(cur.iv.w, 0), d - 1);
+            const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
+            const int i2 = min(max((int)cur.iv.z, 0), d - 1), i3 = min(max((int)cur.iv.w, 0), d - 1);
             *reinterpret_cast<int4 *>(Is + 4 * tid) = make_int4(i0 * MX_XS, i1 * MX_XS, i2 * MX_XS, i3 * MX_XS);
             *reinterpret_cast<uint2 *>(Ws + 2 * tid) = cur.wv;
             if (tid < MX_NLAB * 2) ym[tid] = 0u;
         }
-        prefetch(a, chunk + gridDim.x, tid, nxt);
+        prefetch(a, R, chunk + gridDim.x, tid, lab, u, K, nxt);
         __syncthreads();
         if (tg_lds) {
             for (int e = tid; e < a.nnz; e += MX_THREADS) {
@@ -201,98 +275,86 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         __syncthreads();
 
         int32_t ccol0 = 0, ccol1 = 0, ccol2 = 0, ccol3 = 0;
-#pragma nounroll
+#pragma unroll
         for (int h = 0; h < MX_ROWS; ++h) {
             const int rl = lab + 16 * h;   // row of the chunk this lane serves now
             const int64_t l = l0 + rl;
             const bool valid = l < a.L;
-            float g[4] = {0.f, 0.f, 0.f, 0.f};
+            const float2 mcur = h == 0 ? cur.m[0] : cur.m[1];
+            const float2 vcur = h == 0 ? cur.v[0] : cur.v[1];
+            const float bcur = h == 0 ? cur.b[0] : cur.b[1];
+            const float bmcur = h == 0 ? cur.bm[0] : cur.bm[1];
+            const float bvcur = h == 0 ? cur.bv[0] : cur.bv[1];
+
+            // row data in the lane's slot order: register r <-> slot r ^ K (a row
+            // past L has zero offsets and weights)
+            uint32_t wp[MX_K / 2];
+            uint2 xg[MX_K];
             int32_t c0 = 0, c1 = 0;
-            uint32_t wpair_own = 0u;
-            float2 mcur = make_float2(0.f, 0.f), vcur = make_float2(0.f, 0.f);
-            float bcur = 0.f, bmcur = 0.f, bvcur = 0.f;
-            if (valid) {
-                mcur = *reinterpret_cast<const float2 *>(a.m + l * MX_K + K);
-                vcur = *reinterpret_cast<const float2 *>(a.v + l * MX_K + K);
-                if (a.bias) {
-                    bcur = a.bias[l];
-                    if (u == 0) {
-                        bmcur = a.bm[l];
-                        bvcur = a.bv[l];
-                    }
+#pragma unroll
+            for (int p = 0; p < MX_K / 2; ++p) {
+                const int pp = p ^ (K >> 1);
+                const int2 iv = *reinterpret_cast<const int2 *>(Is + rl * MX_K + 2 * pp);
+                if (p == 0) {
+                    c0 = iv.x / MX_XS;
+                    c1 = iv.y / MX_XS;
                 }
+                xg[2 * p] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
+                xg[2 * p + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
+                wp[p] = Ws[rl * (MX_K / 2) + pp];
             }
-            if (valid) {
-                // row data in the lane's slot order: register r <-> slot r ^ K
-                uint32_t wp[MX_K / 2];
-                uint2 xg[MX_K];
+            const uint32_t wpair_own = wp[0];
+            // forward: repack (b, b+1) pairs of two slots into slot pairs
+            float z[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int p = 0; p < MX_K / 2; ++p) {
-                    const int pp = p ^ (K >> 1);
-                    const int2 iv = *reinterpret_cast<const int2 *>(Is + rl * MX_K + 2 * pp);
-                    if (p == 0) {
-                        c0 = iv.x / MX_XS;
-                        c1 = iv.y / MX_XS;
-                    }
-                    xg[2 * p] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
-                    xg[2 * p + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
-                    wp[p] = Ws[rl * (MX_K / 2) + pp];
-                }
-                wpair_own = wp[0];
-                // forward: repack (b, b+1) pairs of two slots into slot pairs
-                float z[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int p = 0; p < MX_K / 2; ++p) {
+                const uint2 A = xg[2 * p], Bv = xg[2 * p + 1];
+                z[0] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x05040100u), wp[p], z[0]);
+                z[1] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x07060302u), wp[p], z[1]);
+                z[2] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x05040100u), wp[p], z[2]);
+                z[3] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x07060302u), wp[p], z[3]);
+            }
+            // BCE and dlogits for rows 4u..4u+3; zero for padded samples and
+            // rows past L
+            const uint32_t yw = ym[rl * 2 + (u >> 3)] >> ((4 * u) & 31);
+            float g[4];
 #pragma unroll
-                for (int p = 0; p < MX_K / 2; ++p) {
-                    const uint2 A = xg[2 * p], Bv = xg[2 * p + 1];
-                    z[0] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x05040100u), wp[p], z[0]);
-                    z[1] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x07060302u), wp[p], z[1]);
-                    z[2] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x05040100u), wp[p], z[2]);
-                    z[3] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x07060302u), wp[p], z[3]);
-                }
-                // BCE and dlogits for rows 4u..4u+3
-                const uint32_t yw = ym[rl * 2 + (u >> 3)] >> ((4 * u) & 31);
+            for (int e = 0; e < 4; ++e) {
+                const bool live = valid && 4 * u + e < a.B;
+                const float zz = z[e] + bcur;
+                const float y = ((yw >> e) & 1u) ? 1.f : 0.f;
+                const float ex = __expf(-fabsf(zz));
+                const float opx = 1.f + ex;
+                const float r = __builtin_amdgcn_rcpf(opx);
+                const float sig = zz >= 0.f ? r : ex * r;
+                loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __logf(opx) : 0.f;
+                g[e] = live ? a.s * (sig - y) : 0.f;
+            }
+            // dW partials over the lane's rows, slot order r ^ K
+            const uint32_t g01 = pack_bf16(g[0], g[1]), g23 = pack_bf16(g[2], g[3]);
+            float pw[MX_K];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int b = 4 * u + e;
-                    const float zz = z[e] + bcur;
-                    const float y = ((yw >> e) & 1u) ? 1.f : 0.f;
-                    const float ex = __expf(-fabsf(zz));
-                    const float opx = 1.f + ex;
-                    const float r = __builtin_amdgcn_rcpf(opx);
-                    const float sig = zz >= 0.f ? r : ex * r;
-                    if (b < a.B) {
-                        if (a.want_loss) loss_acc += fmaxf(zz, 0.f) - zz * y + __logf(opx);
-                        g[e] = a.s * (sig - y);
-                    }
-                }
-                // dW partials over the lane's rows, slot order r ^ K
-                const uint32_t g01 = pack_bf16(g[0], g[1]), g23 = pack_bf16(g[2], g[3]);
-                float pw[MX_K];
+            for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2(xg[r].x, g01, 0.f));
+            // reduce-scatter over the 16 lanes of the row
 #pragma unroll
-                for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2(xg[r].x, g01, 0.f));
-                // reduce-scatter over the 16 lanes of the row
+            for (int r = 0; r < 16; ++r) pw[r] = add_dpp<DPP_ROW_MIRROR>(pw[r], pw[16 + r]);
 #pragma unroll
-                for (int r = 0; r < 16; ++r) pw[r] = add_dpp<DPP_ROW_MIRROR>(pw[r], pw[16 + r]);
+            for (int r = 0; r < 8; ++r) pw[r] = add_dpp<DPP_ROW_HALF_MIRROR>(pw[r], pw[8 + r]);
 #pragma unroll
-                for (int r = 0; r < 8; ++r) pw[r] = add_dpp<DPP_ROW_HALF_MIRROR>(pw[r], pw[8 + r]);
+            for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_3210>(pw[r], pw[4 + r]);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_3210>(pw[r], pw[4 + r]);
-#pragma unroll
-                for (int r = 0; r < 2; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[2 + r]);
-                // Adam on slots K, K+1
-                {
-                    const int64_t o = l * MX_K + K;
-                    float m0 = mcur.x, m1 = mcur.y, v0 = vcur.x, v1 = vcur.y;
-                    const float w0 = __uint_as_float(wpair_own << 16);
-                    const float w1 = __uint_as_float(wpair_own & 0xffff0000u);
-                    const float n0 = adam_step(w0, pw[0], m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                    const float n1 = adam_step(w1, pw[1], m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                    *reinterpret_cast<float2 *>(a.m + o) = make_float2(m0, m1);
-                    *reinterpret_cast<float2 *>(a.v + o) = make_float2(v0, v1);
-                    const uint32_t packed =
-                        (uint32_t)f32_to_bf16_bits(n0) | ((uint32_t)f32_to_bf16_bits(n1) << 16);
-                    reinterpret_cast<uint32_t *>(a.W)[o >> 1] = packed;
-                }
+            for (int r = 0; r < 2; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[2 + r]);
+            // Adam on slots K, K+1
+            {
+                float m0 = mcur.x, m1 = mcur.y, v0 = vcur.x, v1 = vcur.y;
+                const float w0 = __uint_as_float(wpair_own << 16);
+                const float w1 = __uint_as_float(wpair_own & 0xffff0000u);
+                const float n0 = adam_step(w0, pw[0], m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                const float n1 = adam_step(w1, pw[1], m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                const uint32_t o = (uint32_t)(l * MX_K + K);
+                stf2(R.m, valid ? 4u * o : a.nb_m, make_float2(m0, m1));
+                stf2(R.v, valid ? 4u * o : a.nb_m, make_float2(v0, v1));
+                st32(R.W, valid ? 2u * o : a.nb_W, pack_bf16(n0, n1));
             }
             // bias: sum of g over the 64 rows, lane u == 0 updates
             {
@@ -301,28 +363,24 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 sg = add_dpp<DPP_ROW_HALF_MIRROR>(sg, sg);
                 sg = add_dpp<DPP_QUAD_3210>(sg, sg);
                 sg = add_dpp<DPP_QUAD_1032>(sg, sg);
-                if (valid && u == 0 && a.bias) {
-                    float mm = bmcur, vv = bvcur;
-                    a.bias[l] = adam_step(bcur, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                    a.bm[l] = mm;
-                    a.bv[l] = vv;
-                }
+                float mm = bmcur, vv = bvcur;
+                const float nb = adam_step(bcur, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                const uint32_t ob = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
+                stf(R.b, ob, nb);
+                stf(R.bm, ob, mm);
+                stf(R.bv, ob, vv);
             }
-            // dX inputs: g (zero for invalid rows and padded samples) and the old weights
+            // dX inputs: g and the old weights (a row past L writes zeros at column 0)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) G[(4 * u + e) * MX_NLAB + rl] = f32_to_bf16_bits(g[e]);
-            if (valid) {
-                T[(size_t)c0 * MX_NLAB + rl] = (uint16_t)(wpair_own & 0xffffu);
-                T[(size_t)c1 * MX_NLAB + rl] = (uint16_t)(wpair_own >> 16);
-            }
-            // columns to clear in T once the chunk's matrix-core reads are done
-            // (column 0 stands in for an invalid row: its entry is already zero)
+            for (int e = 0; e < 4; ++e) G[(4 * u + e) * MX_NLAB + rl] = (uint16_t)((e < 2 ? g01 : g23) >> (16 * (e & 1)));
+            T[(size_t)c0 * MX_NLAB + rl] = (uint16_t)(wpair_own & 0xffffu);
+            T[(size_t)c1 * MX_NLAB + rl] = (uint16_t)(wpair_own >> 16);
             if (h == 0) {
-                ccol0 = valid ? c0 : 0;
-                ccol1 = valid ? c1 : 0;
+                ccol0 = c0;
+                ccol1 = c1;
             } else {
-                ccol2 = valid ? c0 : 0;
-                ccol3 = valid ? c1 : 0;
+                ccol2 = c0;
+                ccol3 = c1;
             }
         }
         __syncthreads();
@@ -426,7 +484,11 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.adam = c.adam;
     a.loss_part = loss_part;
     a.dx_part = dx_part;
-    a.want_loss = c.loss_out != nullptr;
+    a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
+    a.nb_W = (uint32_t)(ly.L * MX_K * 2);
+    a.nb_I = (uint32_t)(ly.L * MX_K * 4);
+    a.nb_m = (uint32_t)(ly.L * MX_K * 4);
+    a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
     const size_t shm = sweep_mx_lds(ly.d);
     const MxKernel kern = mx_kernels()[ly.d / 64 - 1];
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),

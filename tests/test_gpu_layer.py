@@ -30,6 +30,9 @@ CASES = {
     # count) with a ragged batch
     "mx64": synth.scaled(W1["c4_bf16_L3M"], L=257, d=64, B=64, name="mx64"),
     "mx320": synth.scaled(W1["c4_bf16_L3M"], L=1003, d=320, B=37, name="mx320"),
+    # more positives per batch (about 1900) than the fast path keeps on chip
+    "mxdense": synth.dataclasses.replace(synth.scaled(W1["c4_bf16_L3M"], L=700, name="mxdense"),
+                                         mean_pos=30.0),
 }
 
 
