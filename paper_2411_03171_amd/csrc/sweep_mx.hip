@@ -1,12 +1,11 @@
 // Fused training step of the fixed fan-in layer for bf16 values, fan-in 32,
-// batches of up to 64 samples and input widths that are a multiple of 64 up to 768
+// batches of up to 64 samples and input widths that are a multiple of 128 up to 768
 // (the gathered forward, BCE, dW, dbias, dX and Adam of Sec. 2.2, in one
 // pass over the [L,k] arrays).
 //
-// Workgroup: 256 threads (4 waves, one per SIMD with 512 registers each),
-// one per CU, persistent over chunks of 32 label rows.  Sixteen lanes serve
-// one row and each lane serves two rows of the chunk in turn; lane u of a row
-// owns batch rows b = 4u .. 4u+3.
+// Workgroup: 512 threads (8 waves, two per SIMD), one per CU, persistent over
+// chunks of 32 label rows.  Sixteen lanes serve one row; lane u of a row owns
+// batch rows b = 4u .. 4u+3.
 //
 //   LDS  Xs [d][64] bf16   the batch transposed (column i is 128 contiguous
 //                          bytes), zero-padded past B
@@ -14,6 +13,7 @@
 //        G  [64][32] bf16  the chunk's dlogits
 //        Is, Ws            the chunk's index rows (as byte offsets into Xs)
 //                          and weight rows
+//        ym [32][2] u32    the chunk's targets as one 64-bit sample mask per row
 //        tg                the batch's positive (label, sample) pairs
 //
 //   1. gather: for each slot, lane u reads the 8 bytes X[4u..4u+3, I[l,j]]
@@ -31,9 +31,9 @@
 //   6. dX: g and the old weights go to G and T, and the matrix cores add
 //      G x T^T (64 x 32 by 32 x d) into a per-workgroup dX held in AGPRs for
 //      the workgroup's whole life; it is written out once at the end.
-// The next chunk's index and weight rows and the optimiser state of its slots
-// are loaded into registers while the current chunk computes; the
-// matrix-core work of a chunk overlaps the VALU work of the next.  All HBM
+// The next chunk's index and weight rows are loaded into registers while the
+// current chunk computes; the matrix-core work of a chunk overlaps the VALU
+// work of the next.  All HBM
 // accesses of the chunk loop are range-checked buffer operations: a row past
 // L reads zeros and its writes are dropped by the hardware, so the loop has no
 // data-dependent branches and the compiler can keep exact counts of
@@ -45,8 +45,7 @@ namespace ffsl {
 
 namespace {
 
-constexpr int MX_THREADS = 256;
-constexpr int MX_ROWS = 2;        // label rows per lane and chunk
+constexpr int MX_THREADS = 512;
 constexpr int MX_NLAB = 32;     // label rows per chunk
 constexpr int MX_K = 32;        // fan-in of this path
 constexpr int MX_NB = 64;       // padded batch
@@ -142,10 +141,8 @@ __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &v
 }
 
 struct Prefetch {
-    uint4 iv;                        // four index words of the chunk's I rows
-    uint2 wv;                        // two weight words of the chunk's W rows
-    float2 m[MX_ROWS], v[MX_ROWS];   // moments of slots K, K+1 of the lane's rows
-    float b[MX_ROWS], bm[MX_ROWS], bv[MX_ROWS];   // bias and its moments
+    uint2 iv;                        // two index words of the chunk's I rows
+    uint32_t wv;                     // one weight word of the chunk's W rows
 };
 
 // the chunk's rows and optimiser state, loaded a chunk ahead of their use; a
@@ -154,33 +151,20 @@ __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_
                                          int K, Prefetch &p) {
     const int64_t l0 = chunk * MX_NLAB;
     const bool live = chunk < a.nchunks;
-    const uint32_t oi = live ? (uint32_t)(l0 * MX_K * 4) + 16u * tid : a.nb_I;
-    const auto iv = __builtin_amdgcn_raw_buffer_load_b128(R.I, oi, 0, 0);
-    p.iv = make_uint4(iv[0], iv[1], iv[2], iv[3]);
-    const uint32_t ow = live ? (uint32_t)(l0 * MX_K * 2) + 8u * tid : a.nb_W;
-    const auto wv = __builtin_amdgcn_raw_buffer_load_b64(R.W, ow, 0, 0);
-    p.wv = make_uint2(wv[0], wv[1]);
-#pragma unroll
-    for (int h = 0; h < MX_ROWS; ++h) {
-        const int64_t l = l0 + lab + 16 * h;
-        const bool ok = live && l < a.L;
-        const uint32_t om = ok ? (uint32_t)(l * MX_K + K) * 4u : a.nb_m;
-        p.m[h] = ldf2(R.m, om);
-        p.v[h] = ldf2(R.v, om);
-        const uint32_t ob = ok ? (uint32_t)l * 4u : a.nb_b;
-        p.b[h] = ldf(R.b, ob);
-        const uint32_t obm = u == 0 ? ob : a.nb_b;
-        p.bm[h] = ldf(R.bm, obm);
-        p.bv[h] = ldf(R.bv, obm);
-    }
+    const uint32_t oi = live ? (uint32_t)(l0 * MX_K * 4) + 8u * tid : a.nb_I;
+    const auto iv = __builtin_amdgcn_raw_buffer_load_b64(R.I, oi, 0, 0);
+    p.iv = make_uint2(iv[0], iv[1]);
+    const uint32_t ow = live ? (uint32_t)(l0 * MX_K * 2) + 4u * tid : a.nb_W;
+    p.wv = ld32(R.W, ow);
 }
 
-// NT = column tiles of 16 per wave: d = 64 * NT (a compile-time width keeps
+
+// NT = column tiles of 16 per wave: d = 128 * NT (a compile-time width keeps
 // the dX accumulators in fixed registers)
 template <int NT>
 __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     extern __shared__ __align__(16) unsigned char lds[];
-    constexpr int d = 64 * NT;
+    constexpr int d = 128 * NT;
     unsigned char *Xs = lds;                                                // d * 128
     uint16_t *T = reinterpret_cast<uint16_t *>(lds + (size_t)d * MX_XS);    // d * 32
     uint16_t *G = T + (size_t)d * MX_NLAB;                                  // 64 * 32
@@ -231,8 +215,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 tg[e] = ((uint32_t)a.tgt_lab[e] << 6) | ((uint32_t)a.tgt_b[e] & 63u);
     }
 
-    // dX accumulators: 4 batch tiles x NT column tiles of 16 per wave
-    const int cbase = wave * (d / 4);
+    // dX accumulators: 4 batch tiles x NT column tiles of 16 per wave (8 waves)
+    const int cbase = wave * (d / 8);
     f32x4 acc[4][NT];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
@@ -251,49 +235,56 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         // become clamped byte offsets of X columns
         {
             const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
-            const int i2 = min(max((int)cur.iv.z, 0), d - 1), i3 = min(max((int)cur.iv.w, 0), d - 1);
-            *reinterpret_cast<int4 *>(Is + 4 * tid) = make_int4(i0 * MX_XS, i1 * MX_XS, i2 * MX_XS, i3 * MX_XS);
-            *reinterpret_cast<uint2 *>(Ws + 2 * tid) = cur.wv;
+            *reinterpret_cast<int2 *>(Is + 2 * tid) = make_int2(i0 * MX_XS, i1 * MX_XS);
+            Ws[tid] = cur.wv;
             if (tid < MX_NLAB * 2) ym[tid] = 0u;
         }
         prefetch(a, R, chunk + gridDim.x, tid, lab, u, K, nxt);
         __syncthreads();
-        if (tg_lds) {
-            for (int e = tid; e < a.nnz; e += MX_THREADS) {
-                const uint32_t key = tg[e];
-                const int64_t ll = (int64_t)(key >> 6) - l0;
-                if (ll >= 0 && ll < MX_NLAB) atomicOr(&ym[ll * 2 + ((key >> 5) & 1)], 1u << (key & 31));
-            }
-        } else {
-            for (int e = tid; e < a.nnz; e += MX_THREADS) {
-                const int64_t ll = (int64_t)a.tgt_lab[e] - l0;
-                const int b = a.tgt_b[e];
-                if (ll >= 0 && ll < MX_NLAB && b >= 0 && b < MX_NB)
-                    atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
+        {
+            // label offsets in 32 bits: a label before the chunk wraps to a large value
+            const uint32_t l0u = (uint32_t)l0;
+            if (tg_lds) {
+                for (int e = tid; e < a.nnz; e += MX_THREADS) {
+                    const uint32_t key = tg[e];
+                    const uint32_t ll = (key >> 6) - l0u;
+                    if (ll < MX_NLAB) atomicOr(&ym[ll * 2 + ((key >> 5) & 1)], 1u << (key & 31));
+                }
+            } else {
+                for (int e = tid; e < a.nnz; e += MX_THREADS) {
+                    const uint32_t ll = (uint32_t)a.tgt_lab[e] - l0u;
+                    const uint32_t b = (uint32_t)a.tgt_b[e];
+                    if (ll < MX_NLAB && b < MX_NB) atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
+                }
             }
         }
         __syncthreads();
 
-        int32_t ccol0 = 0, ccol1 = 0, ccol2 = 0, ccol3 = 0;
-#pragma unroll
-        for (int h = 0; h < MX_ROWS; ++h) {
-            const int rl = lab + 16 * h;   // row of the chunk this lane serves now
+        int32_t c0 = 0, c1 = 0;   // columns of slots K, K+1: cleared in T after the dX step
+        {
+            int rl = lab;            // the row of the chunk this lane serves
+            int k2 = K >> 1;         // pair order of this lane
+            // opaque per chunk, so the per-slot LDS addresses are formed where
+            // they are used instead of being held in registers across chunks
+            asm volatile("" : "+v"(rl), "+v"(k2));
             const int64_t l = l0 + rl;
             const bool valid = l < a.L;
-            const float2 mcur = h == 0 ? cur.m[0] : cur.m[1];
-            const float2 vcur = h == 0 ? cur.v[0] : cur.v[1];
-            const float bcur = h == 0 ? cur.b[0] : cur.b[1];
-            const float bmcur = h == 0 ? cur.bm[0] : cur.bm[1];
-            const float bvcur = h == 0 ? cur.bv[0] : cur.bv[1];
+            // optimiser state of slots K, K+1 and of the bias (zeros past L)
+            const uint32_t om = valid ? (uint32_t)(l * MX_K + K) * 4u : a.nb_m;
+            const float2 mcur = ldf2(R.m, om);
+            const float2 vcur = ldf2(R.v, om);
+            const uint32_t obl = valid ? (uint32_t)l * 4u : a.nb_b;
+            const float bcur = ldf(R.b, obl);
+            const float bmcur = ldf(R.bm, u == 0 ? obl : a.nb_b);
+            const float bvcur = ldf(R.bv, u == 0 ? obl : a.nb_b);
 
             // row data in the lane's slot order: register r <-> slot r ^ K (a row
             // past L has zero offsets and weights)
             uint32_t wp[MX_K / 2];
             uint2 xg[MX_K];
-            int32_t c0 = 0, c1 = 0;
 #pragma unroll
             for (int p = 0; p < MX_K / 2; ++p) {
-                const int pp = p ^ (K >> 1);
+                const int pp = p ^ k2;
                 const int2 iv = *reinterpret_cast<const int2 *>(Is + rl * MX_K + 2 * pp);
                 if (p == 0) {
                     c0 = iv.x / MX_XS;
@@ -372,20 +363,14 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             }
             // dX inputs: g and the old weights (a row past L writes zeros at column 0)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) G[(4 * u + e) * MX_NLAB + rl] = (uint16_t)((e < 2 ? g01 : g23) >> (16 * (e & 1)));
+            for (int e = 0; e < 4; ++e)
+                G[(4 * u + e) * MX_NLAB + rl] = (uint16_t)((e < 2 ? g01 : g23) >> (16 * (e & 1)));
             T[(size_t)c0 * MX_NLAB + rl] = (uint16_t)(wpair_own & 0xffffu);
             T[(size_t)c1 * MX_NLAB + rl] = (uint16_t)(wpair_own >> 16);
-            if (h == 0) {
-                ccol0 = c0;
-                ccol1 = c1;
-            } else {
-                ccol2 = c0;
-                ccol3 = c1;
-            }
         }
         __syncthreads();
         // dX += G (64 x 32) * T^T (32 x d) on the matrix cores; this wave owns
-        // columns [wave*d/4, (wave+1)*d/4).  The fragment reads finish before
+        // columns [wave*d/8, (wave+1)*d/8).  The fragment reads finish before
         // the barrier below; the MFMAs run on while the next chunk starts.
         {
             const int col = lane & 15, kq = lane >> 4;
@@ -405,10 +390,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mt], bfr[nt], acc[mt][nt], 0, 0, 0);
         }
         __syncthreads();
-        T[(size_t)ccol0 * MX_NLAB + lab] = 0;
-        T[(size_t)ccol1 * MX_NLAB + lab] = 0;
-        T[(size_t)ccol2 * MX_NLAB + lab + 16] = 0;
-        T[(size_t)ccol3 * MX_NLAB + lab + 16] = 0;
+        T[(size_t)c0 * MX_NLAB + lab] = 0;
+        T[(size_t)c1 * MX_NLAB + lab] = 0;
         cur = nxt;
     }
 
@@ -440,13 +423,12 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     if (tid == 0) a.loss_part[blockIdx.x] = red[0];
 }
 
-constexpr int MX_NT_MAX = 12;   // widest input: 768 columns
+constexpr int MX_NT_MAX = 6;    // widest input: 768 columns
 
 typedef void (*MxKernel)(const MxArgs);
 const MxKernel *mx_kernels() {
-    static const MxKernel k[MX_NT_MAX] = {k_sweep_mx<1>, k_sweep_mx<2>, k_sweep_mx<3>,  k_sweep_mx<4>,
-                                          k_sweep_mx<5>, k_sweep_mx<6>, k_sweep_mx<7>,  k_sweep_mx<8>,
-                                          k_sweep_mx<9>, k_sweep_mx<10>, k_sweep_mx<11>, k_sweep_mx<12>};
+    static const MxKernel k[MX_NT_MAX] = {k_sweep_mx<1>, k_sweep_mx<2>, k_sweep_mx<3>,
+                                          k_sweep_mx<4>, k_sweep_mx<5>, k_sweep_mx<6>};
     return k;
 }
 
@@ -458,8 +440,8 @@ size_t sweep_mx_lds(int d) {
 }  // namespace
 
 bool sweep_mx_eligible(const Layer &ly, int B, int mode) {
-    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && ly.k == MX_K && B <= MX_NB && ly.d % 64 == 0 &&
-           ly.d >= 64 && ly.d <= 64 * MX_NT_MAX && ly.L < ((int64_t)1 << 25) && sweep_mx_lds(ly.d) <= 160 * 1024;
+    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && ly.k == MX_K && B <= MX_NB && ly.d % 128 == 0 &&
+           ly.d >= 128 && ly.d <= 128 * MX_NT_MAX && ly.L < ((int64_t)1 << 25) && sweep_mx_lds(ly.d) <= 160 * 1024;
 }
 
 int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, int *grid_out) {
@@ -490,7 +472,7 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.nb_m = (uint32_t)(ly.L * MX_K * 4);
     a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
     const size_t shm = sweep_mx_lds(ly.d);
-    const MxKernel kern = mx_kernels()[ly.d / 64 - 1];
+    const MxKernel kern = mx_kernels()[ly.d / 128 - 1];
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
     if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));

@@ -28,7 +28,7 @@ CASES = {
     "b1": synth.scaled(W1["c4_bf16_L3M"], L=513, B=1, name="b1"),
     # the fused bf16 fan-in-32 fast path at other widths (narrowest, odd tile
     # count) with a ragged batch
-    "mx64": synth.scaled(W1["c4_bf16_L3M"], L=257, d=64, B=64, name="mx64"),
+    "mx128": synth.scaled(W1["c4_bf16_L3M"], L=257, d=128, B=64, name="mx128"),
     "mx320": synth.scaled(W1["c4_bf16_L3M"], L=1003, d=320, B=37, name="mx320"),
     # more positives per batch (about 1900) than the fast path keeps on chip
     "mxdense": synth.dataclasses.replace(synth.scaled(W1["c4_bf16_L3M"], L=700, name="mxdense"),
