@@ -190,6 +190,71 @@ FFSL_API int ffsl_set_timing_events(ffsl_layer *layer, void *start, void *stop);
 FFSL_API int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out,
                           void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Dense parts of the architecture around the sparse classifier (Sec. 2.3,
+ * Fig. 1 left).  bf16 operands (FFSL_BF16 bit patterns), fp32 accumulation
+ * on the matrix cores, fp32 outputs unless stated.  Shapes: 1 <= B <=
+ * FFSL_MAX_B; din, dout, d and C are multiples of 8 in [8, 65536] (C up to
+ * 2^20); every bf16 operand is 16-byte aligned.  Scratch lives in the
+ * caller's workspace (sized by the *_workspace_bytes call for the largest B
+ * that will be used); calls sharing a workspace must be ordered.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace of ffsl_dense_gelu_bwd, or 0 for an invalid shape. */
+FFSL_API size_t ffsl_dense_workspace_bytes(int32_t B_max, int32_t din, int32_t dout);
+
+/* Wide intermediate layer between the encoder and the sparse classifier
+ * (Sec. 1 and Sec. 2.3; the activation is not named in the paper -- GELU,
+ * erf form):
+ *   A[b,o] = c[o] + sum_i X[b,i] W1[i,o],   H[b,o] = A * Phi(A)
+ *   X  [B,din] bf16;  W1 [din,dout] bf16;  c [dout] fp32, nullable
+ *   A_out [B,dout] fp32 (kept for the backward);  H_out [B,dout] bf16 */
+FFSL_API int ffsl_dense_gelu_fwd(const void *X, int32_t B, int32_t din, int32_t dout,
+                        const void *W1, const float *c, float *A_out, void *H_out,
+                        void *stream);
+
+/* Backward of ffsl_dense_gelu_fwd for the upstream gradient dH [B,dout]
+ * fp32 (the sparse layer's dX):
+ *   dA = dH * (Phi(A) + A phi(A))           (fp32, rounded to bf16 for the products)
+ *   dW1[i,o] = sum_b X[b,i] dA[b,o]          -> dW1 [din,dout] fp32
+ *   dc[o]    = sum_b dA[b,o]                 -> dc [dout] fp32, nullable
+ *   dX[b,i]  = sum_o dA[b,o] W1[i,o]         -> dX_out [B,din] fp32, nullable;
+ *                                               added into with FFSL_ACCUM_DX */
+FFSL_API int ffsl_dense_gelu_bwd(const void *X, int32_t B, int32_t din, int32_t dout,
+                        const void *W1, const float *A, const float *dH, float *dW1,
+                        float *dc, float *dX_out, uint32_t flags, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/* Workspace of ffsl_aux_bce_fwd_bwd, or 0 for an invalid shape. */
+FFSL_API size_t ffsl_aux_workspace_bytes(int32_t B_max, int32_t d, int32_t C);
+
+/* Auxiliary meta-classifier over C label clusters (Sec. 2.3; its appendix on
+ * random clusters: a random label-to-cluster map works as well as k-means,
+ * so label l belongs to cluster l mod C), trained with its own BCE loss next
+ * to the sparse layer's:
+ *   Za[b,c] = ca[c] + sum_i X[b,i] Wa[i,c]
+ *   ya[b,c] = 1 iff some positive l of sample b has l mod C == c
+ *   *loss_out = s * sum BCE-with-logits(Za, ya)    (+= with FFSL_ACCUM_LOSS)
+ *   dZ = s * (sigmoid(Za) - ya)                    (fp32, bf16 for the products)
+ *   dWa[i,c] = sum_b X[b,i] dZ[b,c];  dca[c] = sum_b dZ[b,c]
+ *   dX[b,i] = sum_c dZ[b,c] Wa[i,c]                (+= with FFSL_ACCUM_DX)
+ *   X [B,d] bf16; Wa [d,C] bf16; ca [C] fp32 nullable; tgt_off/tgt_lab as in
+ *   ffsl_forward_loss (negative labels are ignored); loss_out, dca, dX_out,
+ *   logits_out (fp32 [B,C], for tests) nullable; dWa [d,C] fp32. */
+FFSL_API int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C,
+                         const void *Wa, const float *ca, const int32_t *tgt_off,
+                         const int32_t *tgt_lab, int32_t nnz, float s, float *loss_out,
+                         float *dWa, float *dca, float *dX_out, float *logits_out,
+                         uint32_t flags, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/* Adam / AdamW step, as ffsl_adam_step, on a flat parameter array of n
+ * values (value_dtype FFSL_F32 or FFSL_BF16) with fp32 gradient and moments:
+ * the dense layers' weights and biases. */
+FFSL_API int ffsl_adam_dense(void *param, int32_t value_dtype, const float *grad, float *m,
+                    float *v, int64_t n, int64_t t, float lr, float beta1, float beta2,
+                    float eps, float wd, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -55,4 +55,18 @@ int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st) {
     return check_launch("adam");
 }
 
+// the same update over a flat parameter array (the dense layers' weights and
+// biases)
+int launch_adam_flat(void *p, int vt, const float *g, float *m, float *v, int64_t n, const AdamParams &ap,
+                     int num_cu, hipStream_t st) {
+    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, (int64_t)num_cu * 16));
+    if (vt == FFSL_BF16)
+        hipLaunchKernelGGL(k_adam<FFSL_BF16>, dim3(blocks), dim3(256), 0, st, p, g, m, v, n, nullptr, nullptr,
+                           nullptr, nullptr, (int64_t)0, ap);
+    else
+        hipLaunchKernelGGL(k_adam<FFSL_F32>, dim3(blocks), dim3(256), 0, st, p, g, m, v, n, nullptr, nullptr,
+                           nullptr, nullptr, (int64_t)0, ap);
+    return check_launch("adam_flat");
+}
+
 }  // namespace ffsl

@@ -106,6 +106,30 @@ static int check_adam(int64_t t, float lr, float b1, float b2, float eps, float 
     return FFSL_OK;
 }
 
+
+static int check_width(const char *name, int64_t x, int64_t hi) {
+    if (x < 8 || x > hi || x % 8 != 0)
+        return fail(FFSL_EINVAL, "%s must be a multiple of 8 in [8,%lld] (got %lld)", name, (long long)hi,
+                    (long long)x);
+    return FFSL_OK;
+}
+
+static int check_aligned16(const char *name, const void *p) {
+    if (!p) return fail(FFSL_EINVAL, "%s is null", name);
+    if (reinterpret_cast<uintptr_t>(p) & 15u) return fail(FFSL_EINVAL, "%s must be 16-byte aligned", name);
+    return FFSL_OK;
+}
+
+static int check_dense_batch(int32_t B) {
+    if (B < 1 || B > FFSL_MAX_B) return fail(FFSL_EINVAL, "B must be in [1,%d] (got %d)", FFSL_MAX_B, B);
+    return FFSL_OK;
+}
+
+static int current_cu_count(int *cu) {
+    int dev = 0;
+    return device_cu_count(cu, &dev);
+}
+
 }  // namespace ffsl
 
 using namespace ffsl;
@@ -295,6 +319,93 @@ int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out, void *stream
     if (!layer) return fail(FFSL_EINVAL, "layer is null");
     if (!bad_rows_out) return fail(FFSL_EINVAL, "bad_rows_out is null");
     return launch_validate(layer->ly, bad_rows_out, static_cast<hipStream_t>(stream));
+}
+
+
+size_t ffsl_dense_workspace_bytes(int32_t B_max, int32_t din, int32_t dout) {
+    g_err.clear();
+    if (check_dense_batch(B_max) || check_width("din", din, 65536) || check_width("dout", dout, 65536)) return 0;
+    return dense_ws(B_max, din, dout).total;
+}
+
+int ffsl_dense_gelu_fwd(const void *X, int32_t B, int32_t din, int32_t dout, const void *W1, const float *c,
+                        float *A_out, void *H_out, void *stream) {
+    g_err.clear();
+    int rc;
+    if ((rc = check_dense_batch(B)) || (rc = check_width("din", din, 65536)) ||
+        (rc = check_width("dout", dout, 65536)) || (rc = check_aligned16("X", X)) ||
+        (rc = check_aligned16("W1", W1)))
+        return rc;
+    if (!A_out || !H_out) return fail(FFSL_EINVAL, "A_out and H_out are required");
+    return launch_dense_gelu_fwd(static_cast<const uint16_t *>(X), B, din, dout, static_cast<const uint16_t *>(W1),
+                                 c, A_out, static_cast<uint16_t *>(H_out), static_cast<hipStream_t>(stream));
+}
+
+int ffsl_dense_gelu_bwd(const void *X, int32_t B, int32_t din, int32_t dout, const void *W1, const float *A,
+                        const float *dH, float *dW1, float *dc, float *dX_out, uint32_t flags, void *workspace,
+                        size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    int rc;
+    if ((rc = check_dense_batch(B)) || (rc = check_width("din", din, 65536)) ||
+        (rc = check_width("dout", dout, 65536)) || (rc = check_aligned16("X", X)) ||
+        (rc = check_aligned16("W1", W1)))
+        return rc;
+    if (!A || !dH || !dW1) return fail(FFSL_EINVAL, "A, dH and dW1 are required");
+    if (!workspace) return fail(FFSL_EINVAL, "workspace is null");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return fail(FFSL_EINVAL, "workspace must be 256-byte aligned");
+    const size_t need = dense_ws(B, din, dout).total;
+    if (workspace_bytes < need)
+        return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return launch_dense_gelu_bwd(static_cast<const uint16_t *>(X), B, din, dout, static_cast<const uint16_t *>(W1),
+                                 A, dH, dW1, dc, dX_out, (flags & FFSL_ACCUM_DX) != 0,
+                                 static_cast<char *>(workspace), static_cast<hipStream_t>(stream));
+}
+
+size_t ffsl_aux_workspace_bytes(int32_t B_max, int32_t d, int32_t C) {
+    g_err.clear();
+    if (check_dense_batch(B_max) || check_width("d", d, 65536) || check_width("C", C, 1 << 20)) return 0;
+    return aux_ws(B_max, d, C).total;
+}
+
+int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C, const void *Wa, const float *ca,
+                         const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz, float s, float *loss_out,
+                         float *dWa, float *dca, float *dX_out, float *logits_out, uint32_t flags, void *workspace,
+                         size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    int rc;
+    if ((rc = check_dense_batch(B)) || (rc = check_width("d", d, 65536)) || (rc = check_width("C", C, 1 << 20)) ||
+        (rc = check_aligned16("X", X)) || (rc = check_aligned16("Wa", Wa)))
+        return rc;
+    if (!tgt_off) return fail(FFSL_EINVAL, "tgt_off is null");
+    if (nnz < 0) return fail(FFSL_EINVAL, "nnz must be >= 0");
+    if (nnz > 0 && !tgt_lab) return fail(FFSL_EINVAL, "tgt_lab is null");
+    if (!dWa) return fail(FFSL_EINVAL, "dWa is required");
+    if (!workspace) return fail(FFSL_EINVAL, "workspace is null");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return fail(FFSL_EINVAL, "workspace must be 256-byte aligned");
+    const size_t need = aux_ws(B, d, C).total;
+    if (workspace_bytes < need)
+        return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return launch_aux_bce(static_cast<const uint16_t *>(X), B, d, C, static_cast<const uint16_t *>(Wa), ca, tgt_off,
+                          tgt_lab, nnz, s, loss_out, dWa, dca, dX_out, logits_out, (flags & FFSL_ACCUM_DX) != 0,
+                          (flags & FFSL_ACCUM_LOSS) != 0, static_cast<char *>(workspace),
+                          static_cast<hipStream_t>(stream));
+}
+
+int ffsl_adam_dense(void *param, int32_t value_dtype, const float *grad, float *m, float *v, int64_t n, int64_t t,
+                    float lr, float beta1, float beta2, float eps, float wd, void *stream) {
+    g_err.clear();
+    if (!param || !grad || !m || !v) return fail(FFSL_EINVAL, "param, grad, m and v are required");
+    if (value_dtype != FFSL_F32 && value_dtype != FFSL_BF16)
+        return fail(FFSL_EUNSUPPORTED, "value_dtype must be FFSL_F32 or FFSL_BF16");
+    if (n < 1) return fail(FFSL_EINVAL, "n must be >= 1");
+    AdamParams ap{};
+    int rc = check_adam(t, lr, beta1, beta2, eps, wd, &ap);
+    if (rc) return rc;
+    int cu = 0;
+    if ((rc = current_cu_count(&cu))) return rc;
+    return launch_adam_flat(param, value_dtype, grad, m, v, n, ap, cu, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -1,0 +1,434 @@
+// Dense parts of the architecture around the sparse classifier (Sec. 2.3,
+// Fig. 1 left): the wide intermediate layer H = GELU(X W1 + c) with its
+// backward, and the auxiliary cluster classifier Za = X Wa + ca with its BCE
+// loss and backward.  All products run on the matrix cores through one tiled
+// GEMM with fused epilogues:
+//
+//   C[M,N] = sum_k A(m,k) B(k,n),   A(m,k) = TA ? A[k*lda+m] : A[m*lda+k]
+//                                   B(k,n) = TB ? B[n*ldb+k] : B[k*ldb+n]
+//
+// bf16 operands, fp32 accumulation.  A workgroup of 256 threads computes a
+// 64 x 64 tile; each wave a 32 x 32 quarter with 2 x 2 v_mfma_f32_16x16x32_bf16
+// per 32-deep K step.  Both operands are staged into LDS K-contiguous, so
+// every fragment is one 16-byte LDS read whatever the source layout.  Long K
+// (the dX products) is split over blockIdx.z into fp32 partials that a second
+// kernel sums in a fixed order.
+#include <math.h>
+
+#include <algorithm>
+
+#include "ffsl_internal.h"
+
+namespace ffsl {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int GT = 64;        // tile edge in M and N
+constexpr int GK = 32;        // K per stage
+constexpr int GKP = GK + 8;   // LDS row in elements (padded against bank conflicts)
+
+enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2, EPI_BCE = 3 };
+
+struct GemmArgs {
+    const uint16_t *A;
+    int64_t lda;
+    const uint16_t *B;
+    int64_t ldb;
+    int M, N, K, kchunk;
+    float *C;                 // STORE: C[m*N+n]; PARTIAL: C[(z*M+m)*N+n]; GELU: pre-activation; BCE: dZ
+    const float *bias;        // GELU, BCE: per-column bias (nullable)
+    uint16_t *H;              // GELU: bf16 activation
+    const uint32_t *ymask;    // BCE: targets, one bit per (m, n), ywords words per row
+    int ywords;
+    float s;                  // BCE: loss scale
+    float *Zout;              // BCE: nullable logits
+    float *loss_part;         // BCE: one partial per workgroup
+};
+
+// Stage a 64-row x 32-deep tile of one operand into S[row][k].
+//   KC = true : source stored row-major with k contiguous, src[r*ld + k]
+//   KC = false: source stored with the rows contiguous,   src[k*ld + r]
+// Out-of-range rows and k read as zero.  Callers guarantee that the contiguous
+// extent (K for KC, the row count otherwise) is a multiple of 8 and that
+// src and ld keep every 8-element group 16-byte aligned.
+template <bool KC>
+__device__ __forceinline__ void stage(uint16_t (*S)[GKP], const uint16_t *src, int64_t ld, int r0, int R,
+                                      int k0, int kend, int tid) {
+    if (KC) {
+        const int r = tid >> 2, kc = (tid & 3) * 8;
+        const int gr = r0 + r, gk = k0 + kc;
+        uint4 q = make_uint4(0u, 0u, 0u, 0u);
+        if (gr < R && gk < kend) q = *reinterpret_cast<const uint4 *>(src + (int64_t)gr * ld + gk);
+        *reinterpret_cast<uint4 *>(&S[r][kc]) = q;
+    } else {
+        const int kr = tid >> 3, rc = (tid & 7) * 8;
+        const int gk = k0 + kr, gr = r0 + rc;
+        uint4 q = make_uint4(0u, 0u, 0u, 0u);
+        if (gk < kend && gr < R) q = *reinterpret_cast<const uint4 *>(src + (int64_t)gk * ld + gr);
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            S[rc + 2 * e][kr] = (uint16_t)(w[e] & 0xffffu);
+            S[rc + 2 * e + 1][kr] = (uint16_t)(w[e] >> 16);
+        }
+    }
+}
+
+__device__ __forceinline__ float gelu_cdf(float a) { return 0.5f * (1.f + erff(a * 0.70710678118654752f)); }
+
+template <bool TA, bool TB, int EPI>
+__global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
+    __shared__ __align__(16) uint16_t As[GT][GKP];
+    __shared__ __align__(16) uint16_t Bs[GT][GKP];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1, col = lane & 15, kq = lane >> 4;
+    const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
+    const int kbeg = blockIdx.z * g.kchunk, kend = min(g.K, kbeg + g.kchunk);
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = kbeg; k0 < kend; k0 += GK) {
+        stage<!TA>(As, g.A, g.lda, m0, g.M, k0, kend, tid);
+        stage<TB>(Bs, g.B, g.ldb, n0, g.N, k0, kend, tid);
+        __syncthreads();
+        bf16x8 af[2], bv[2];
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+            af[mi] = *reinterpret_cast<const bf16x8 *>(&As[32 * wm + 16 * mi + col][8 * kq]);
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+            bv[ni] = *reinterpret_cast<const bf16x8 *>(&Bs[32 * wn + 16 * ni + col][8 * kq]);
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mi], bv[ni], acc[mi][ni], 0, 0, 0);
+        __syncthreads();
+    }
+
+    // accumulator element r of tile (mi, ni) is C[row 4*kq + r][column col]
+    float lsum = 0.f;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + 32 * wm + 16 * mi + 4 * kq + r;
+                const int n = n0 + 32 * wn + 16 * ni + col;
+                if (m >= g.M || n >= g.N) continue;
+                const float x = acc[mi][ni][r];
+                const int64_t o = (int64_t)m * g.N + n;
+                if constexpr (EPI == EPI_STORE) {
+                    g.C[o] = x;
+                } else if constexpr (EPI == EPI_PARTIAL) {
+                    g.C[(int64_t)blockIdx.z * g.M * g.N + o] = x;
+                } else if constexpr (EPI == EPI_GELU) {
+                    const float a = x + (g.bias ? g.bias[n] : 0.f);
+                    g.C[o] = a;
+                    g.H[o] = f32_to_bf16_bits(a * gelu_cdf(a));
+                } else {
+                    const float z = x + (g.bias ? g.bias[n] : 0.f);
+                    const float y = ((g.ymask[(int64_t)m * g.ywords + (n >> 5)] >> (n & 31)) & 1u) ? 1.f : 0.f;
+                    const float ex = expf(-fabsf(z));
+                    lsum += fmaxf(z, 0.f) - z * y + log1pf(ex);
+                    const float sig = z >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
+                    g.C[o] = g.s * (sig - y);
+                    if (g.Zout) g.Zout[o] = z;
+                }
+            }
+    if constexpr (EPI == EPI_BCE) {
+        __shared__ float red[256];
+        red[tid] = lsum;
+        __syncthreads();
+        for (int st = 128; st > 0; st >>= 1) {
+            if (tid < st) red[tid] += red[tid + st];
+            __syncthreads();
+        }
+        if (tid == 0) g.loss_part[blockIdx.y * gridDim.x + blockIdx.x] = g.s * red[0];
+    }
+}
+
+// dA = dH * GELU'(A), GELU'(a) = Phi(a) + a phi(a); the bf16 copy feeds the
+// two products, the fp32 column sums are dc.  One thread per column.
+__global__ void __launch_bounds__(256) k_gelu_bwd_cols(const float *A, const float *dH, int B, int N,
+                                                       uint16_t *dA16, float *dc) {
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= N) return;
+    float sum = 0.f;
+    for (int b = 0; b < B; ++b) {
+        const int64_t o = (int64_t)b * N + n;
+        const float a = A[o];
+        const float pdf = 0.39894228040143268f * expf(-0.5f * a * a);
+        const float da = dH[o] * (gelu_cdf(a) + a * pdf);
+        dA16[o] = f32_to_bf16_bits(da);
+        sum += da;
+    }
+    if (dc) dc[n] = sum;
+}
+
+// column sums of an fp32 [B,N] matrix (nullable) and its bf16 copy
+__global__ void __launch_bounds__(256) k_cols_cvt(const float *Z, int B, int N, uint16_t *Z16, float *csum) {
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= N) return;
+    float sum = 0.f;
+    for (int b = 0; b < B; ++b) {
+        const int64_t o = (int64_t)b * N + n;
+        const float z = Z[o];
+        Z16[o] = f32_to_bf16_bits(z);
+        sum += z;
+    }
+    if (csum) csum[n] = sum;
+}
+
+// out[e] (+)= sum_z P[z][e], the split-K partials in ascending z
+__global__ void __launch_bounds__(256) k_split_sum(const float *P, int S, int64_t MN, float *out, int accum) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < MN; e += stride) {
+        float s = accum ? out[e] : 0.f;
+        for (int z = 0; z < S; ++z) s += P[(int64_t)z * MN + e];
+        out[e] = s;
+    }
+}
+
+// *loss (+)= sum of n partials, one workgroup
+__global__ void __launch_bounds__(256) k_sum_partials(const float *part, int n, float *loss, int accum) {
+    __shared__ float red[256];
+    float s = 0.f;
+    for (int i = threadIdx.x; i < n; i += 256) s += part[i];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = (accum ? *loss : 0.f) + red[0];
+}
+
+__global__ void __launch_bounds__(256) k_fill_u32(uint32_t *p, int64_t n, uint32_t x) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) p[e] = x;
+}
+
+// cluster targets: bit (b, l mod C) for every positive l of sample b; the
+// sample of CSR entry e is found by binary search in the offsets
+__global__ void __launch_bounds__(256) k_aux_targets(const int32_t *off, const int32_t *lab, int B, int nnz,
+                                                     int C, int words, uint32_t *ymask) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= nnz) return;
+    int lo = 0, hi = B;   // the last b with off[b] <= e
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= e) lo = mid; else hi = mid;
+    }
+    const int l = lab[e];
+    if (l < 0) return;
+    const int c = l % C;
+    atomicOr(&ymask[(int64_t)lo * words + (c >> 5)], 1u << (c & 31));
+}
+
+template <bool TA, bool TB, int EPI>
+int gemm(const GemmArgs &g, int splits, hipStream_t st) {
+    dim3 grid((g.N + GT - 1) / GT, (g.M + GT - 1) / GT, splits);
+    hipLaunchKernelGGL((k_gemm<TA, TB, EPI>), grid, dim3(256), 0, st, g);
+    return check_launch("gemm");
+}
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// split count and K chunk of a long-K product: chunks of at least 256,
+// at most 16 splits
+void split_k(int K, int *splits, int *kchunk) {
+    int s = std::max(1, std::min(16, K / 512));
+    int kc = (K + s - 1) / s;
+    kc = (kc + GK - 1) / GK * GK;
+    s = (K + kc - 1) / kc;
+    *splits = s;
+    *kchunk = kc;
+}
+
+int blocks_for(int64_t n) { return (int)std::min<int64_t>((n + 255) / 256, 4096); }
+
+}  // namespace
+
+DenseWs dense_ws(int B_max, int din, int dout) {
+    DenseWs w{};
+    int S, kc;
+    split_k(dout, &S, &kc);
+    size_t off = 0;
+    w.dA16 = off;
+    off = al256(off + sizeof(uint16_t) * (size_t)B_max * dout);
+    w.dx_part = off;
+    off = al256(off + sizeof(float) * (size_t)S * B_max * din);
+    w.total = off;
+    return w;
+}
+
+AuxWs aux_ws(int B_max, int d, int C) {
+    AuxWs w{};
+    int S, kc;
+    split_k(C, &S, &kc);
+    const int words = (C + 31) / 32;
+    size_t off = 0;
+    w.ymask = off;
+    off = al256(off + sizeof(uint32_t) * (size_t)B_max * words);
+    w.dz = off;
+    off = al256(off + sizeof(float) * (size_t)B_max * C);
+    w.dz16 = off;
+    off = al256(off + sizeof(uint16_t) * (size_t)B_max * C);
+    w.loss_part = off;
+    off = al256(off + sizeof(float) * (size_t)((C + GT - 1) / GT) * ((B_max + GT - 1) / GT));
+    w.dx_part = off;
+    off = al256(off + sizeof(float) * (size_t)S * B_max * d);
+    w.total = off;
+    return w;
+}
+
+int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *c,
+                          float *A_out, uint16_t *H_out, hipStream_t st) {
+    GemmArgs g{};
+    g.A = X;
+    g.lda = din;
+    g.B = W1;
+    g.ldb = dout;
+    g.M = B;
+    g.N = dout;
+    g.K = din;
+    g.kchunk = (din + GK - 1) / GK * GK;
+    g.C = A_out;
+    g.bias = c;
+    g.H = H_out;
+    return gemm<false, false, EPI_GELU>(g, 1, st);
+}
+
+int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *A,
+                          const float *dH, float *dW1, float *dc, float *dX, bool accum, char *ws,
+                          hipStream_t st) {
+    const DenseWs w = dense_ws(B, din, dout);
+    uint16_t *dA16 = reinterpret_cast<uint16_t *>(ws + w.dA16);
+    hipLaunchKernelGGL(k_gelu_bwd_cols, dim3((dout + 255) / 256), dim3(256), 0, st, A, dH, B, dout, dA16, dc);
+    int rc = check_launch("gelu_bwd_cols");
+    if (rc) return rc;
+    // dW1[i,o] = sum_b X[b,i] dA[b,o]: A(m=i, k=b) = X[b*din+i] (TA), B(k=b, n=o) = dA[b*dout+o]
+    GemmArgs g{};
+    g.A = X;
+    g.lda = din;
+    g.B = dA16;
+    g.ldb = dout;
+    g.M = din;
+    g.N = dout;
+    g.K = B;
+    g.kchunk = (B + GK - 1) / GK * GK;
+    g.C = dW1;
+    rc = gemm<true, false, EPI_STORE>(g, 1, st);
+    if (rc || !dX) return rc;
+    // dX[b,i] = sum_o dA[b,o] W1[i,o]: A(m=b, k=o) = dA[b*dout+o], B(k=o, n=i) = W1[i*dout+o] (TB)
+    int S, kc;
+    split_k(dout, &S, &kc);
+    float *P = reinterpret_cast<float *>(ws + w.dx_part);
+    GemmArgs h{};
+    h.A = dA16;
+    h.lda = dout;
+    h.B = W1;
+    h.ldb = dout;
+    h.M = B;
+    h.N = din;
+    h.K = dout;
+    h.kchunk = kc;
+    h.C = P;
+    rc = gemm<false, true, EPI_PARTIAL>(h, S, st);
+    if (rc) return rc;
+    const int64_t MN = (int64_t)B * din;
+    hipLaunchKernelGGL(k_split_sum, dim3(blocks_for(MN)), dim3(256), 0, st, P, S, MN, dX, accum ? 1 : 0);
+    return check_launch("split_sum");
+}
+
+int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, const float *ca,
+                   const int32_t *off, const int32_t *lab, int nnz, float s, float *loss, float *dWa, float *dca,
+                   float *dX, float *Zout, bool accum_dx, bool accum_loss, char *ws, hipStream_t st) {
+    const AuxWs w = aux_ws(B, d, C);
+    const int words = (C + 31) / 32;
+    uint32_t *ym = reinterpret_cast<uint32_t *>(ws + w.ymask);
+    float *dz = reinterpret_cast<float *>(ws + w.dz);
+    uint16_t *dz16 = reinterpret_cast<uint16_t *>(ws + w.dz16);
+    float *lp = reinterpret_cast<float *>(ws + w.loss_part);
+    const int64_t nm = (int64_t)B * words;
+    hipLaunchKernelGGL(k_fill_u32, dim3(blocks_for(nm)), dim3(256), 0, st, ym, nm, 0u);
+    int rc = check_launch("fill");
+    if (rc) return rc;
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_aux_targets, dim3((nnz + 255) / 256), dim3(256), 0, st, off, lab, B, nnz, C, words,
+                           ym);
+        rc = check_launch("aux_targets");
+        if (rc) return rc;
+    }
+    // Za = X Wa + ca with the BCE epilogue: A(m=b, k=i) = X[b*d+i], B(k=i, n=c) = Wa[i*C+c]
+    GemmArgs g{};
+    g.A = X;
+    g.lda = d;
+    g.B = Wa;
+    g.ldb = C;
+    g.M = B;
+    g.N = C;
+    g.K = d;
+    g.kchunk = (d + GK - 1) / GK * GK;
+    g.C = dz;
+    g.bias = ca;
+    g.ymask = ym;
+    g.ywords = words;
+    g.s = s;
+    g.Zout = Zout;
+    g.loss_part = lp;
+    rc = gemm<false, false, EPI_BCE>(g, 1, st);
+    if (rc) return rc;
+    const int nparts = ((C + GT - 1) / GT) * ((B + GT - 1) / GT);
+    if (loss) {
+        hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, st, lp, nparts, loss, accum_loss ? 1 : 0);
+        rc = check_launch("sum_partials");
+        if (rc) return rc;
+    }
+    hipLaunchKernelGGL(k_cols_cvt, dim3((C + 255) / 256), dim3(256), 0, st, dz, B, C, dz16, dca);
+    rc = check_launch("cols_cvt");
+    if (rc) return rc;
+    // dWa[i,c] = sum_b X[b,i] dZ[b,c]
+    GemmArgs h{};
+    h.A = X;
+    h.lda = d;
+    h.B = dz16;
+    h.ldb = C;
+    h.M = d;
+    h.N = C;
+    h.K = B;
+    h.kchunk = (B + GK - 1) / GK * GK;
+    h.C = dWa;
+    rc = gemm<true, false, EPI_STORE>(h, 1, st);
+    if (rc || !dX) return rc;
+    // dXa[b,i] = sum_c dZ[b,c] Wa[i,c], added into dX when asked
+    int S, kc;
+    split_k(C, &S, &kc);
+    float *P = reinterpret_cast<float *>(ws + w.dx_part);
+    GemmArgs q{};
+    q.A = dz16;
+    q.lda = C;
+    q.B = Wa;
+    q.ldb = C;
+    q.M = B;
+    q.N = d;
+    q.K = C;
+    q.kchunk = kc;
+    q.C = P;
+    rc = gemm<false, true, EPI_PARTIAL>(q, S, st);
+    if (rc) return rc;
+    const int64_t MN = (int64_t)B * d;
+    hipLaunchKernelGGL(k_split_sum, dim3(blocks_for(MN)), dim3(256), 0, st, P, S, MN, dX, accum_dx ? 1 : 0);
+    return check_launch("split_sum");
+}
+
+}  // namespace ffsl

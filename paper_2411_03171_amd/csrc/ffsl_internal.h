@@ -103,5 +103,35 @@ int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
                uint8_t *mask, int32_t *exhausted, hipStream_t st);
 int launch_validate(const Layer &ly, int32_t *bad_rows, hipStream_t st);
+int launch_adam_flat(void *p, int vt, const float *g, float *m, float *v, int64_t n, const AdamParams &ap,
+                     int num_cu, hipStream_t st);
+
+// ---------------------------------------------------------------- dense parts
+
+// workspace of the intermediate layer's backward (byte offsets, 256-aligned)
+struct DenseWs {
+    size_t dA16;     // bf16 [B_max, dout]
+    size_t dx_part;  // fp32 [splits, B_max, din]
+    size_t total;
+};
+// workspace of the auxiliary head
+struct AuxWs {
+    size_t ymask;      // u32 [B_max, ceil(C/32)] cluster targets
+    size_t dz;         // fp32 [B_max, C]
+    size_t dz16;       // bf16 [B_max, C]
+    size_t loss_part;  // fp32, one per forward tile
+    size_t dx_part;    // fp32 [splits, B_max, d]
+    size_t total;
+};
+DenseWs dense_ws(int B_max, int din, int dout);
+AuxWs aux_ws(int B_max, int d, int C);
+int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *c,
+                          float *A_out, uint16_t *H_out, hipStream_t st);
+int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *A,
+                          const float *dH, float *dW1, float *dc, float *dX, bool accum, char *ws,
+                          hipStream_t st);
+int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, const float *ca,
+                   const int32_t *off, const int32_t *lab, int nnz, float s, float *loss, float *dWa, float *dca,
+                   float *dX, float *Zout, bool accum_dx, bool accum_loss, char *ws, hipStream_t st);
 
 }  // namespace ffsl

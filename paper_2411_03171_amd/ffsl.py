@@ -36,6 +36,14 @@ SIGNATURES = {
     "ffsl_set_update": (_int, [_vp, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_validate_indices": (_int, [_vp, _vp, _vp]),
     "ffsl_set_timing_events": (_int, [_vp, _vp, _vp]),
+    "ffsl_dense_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "ffsl_dense_gelu_fwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "ffsl_dense_gelu_bwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp, _sz,
+                                   _vp]),
+    "ffsl_aux_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "ffsl_aux_bce_fwd_bwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _f32, _vp, _vp, _vp,
+                                    _vp, _vp, _u32, _vp, _sz, _vp]),
+    "ffsl_adam_dense": (_int, [_vp, _i32, _vp, _vp, _vp, _i64, _i64, _f32, _f32, _f32, _f32, _f32, _vp]),
 }
 
 _lib = None
@@ -234,3 +242,96 @@ class SparseLayer:
         bad = torch.zeros(1, dtype=torch.int32, device=self.W.device)
         _check(load().ffsl_validate_indices(self._handle, _ptr(bad), _stream(torch)))
         return bad
+
+
+# ---------------------------------------------------------------------------
+# dense parts: the intermediate GELU layer and the auxiliary cluster head
+
+
+def _bf16_2d(t, name):
+    import torch
+    if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != 2 or not t.is_contiguous():
+        raise TypeError("%s must be a contiguous 2-D bfloat16 CUDA tensor" % name)
+    return t
+
+
+def _workspace(torch, nbytes, dev):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
+
+
+def dense_gelu_fwd(X, W1, c=None):
+    """H = GELU(X W1 + c) (bf16) and the pre-activation A (fp32) for the backward."""
+    import torch
+    lib = load()
+    _bf16_2d(X, "X")
+    _bf16_2d(W1, "W1")
+    B, din = X.shape
+    dout = W1.shape[1]
+    A = torch.empty((B, dout), dtype=torch.float32, device=X.device)
+    H = torch.empty((B, dout), dtype=torch.bfloat16, device=X.device)
+    _check(lib.ffsl_dense_gelu_fwd(_ptr(X), B, din, dout, _ptr(W1), _ptr(c), _ptr(A), _ptr(H),
+                                   _stream(torch)))
+    return A, H
+
+
+def dense_gelu_bwd(X, W1, A, dH, want_dc=True, dX_out=None, flags=0):
+    """dW1, dc and dX of the intermediate layer for the upstream gradient dH (fp32)."""
+    import torch
+    lib = load()
+    B, din = X.shape
+    dout = W1.shape[1]
+    dev = X.device
+    dW1 = torch.empty((din, dout), dtype=torch.float32, device=dev)
+    dc = torch.empty(dout, dtype=torch.float32, device=dev) if want_dc else None
+    dX = dX_out if dX_out is not None else torch.empty((B, din), dtype=torch.float32, device=dev)
+    ws_bytes = lib.ffsl_dense_workspace_bytes(B, din, dout)
+    if ws_bytes == 0:
+        raise FfslError(FFSL_EINVAL, lib.ffsl_last_error().decode())
+    ws = _workspace(torch, ws_bytes, dev)
+    _check(lib.ffsl_dense_gelu_bwd(_ptr(X), B, din, dout, _ptr(W1), _ptr(A), _ptr(dH), _ptr(dW1), _ptr(dc),
+                                   _ptr(dX), flags, _ptr(ws), ws.numel(), _stream(torch)))
+    return dW1, dc, dX
+
+
+def aux_bce_fwd_bwd(X, Wa, ca, off, lab, s=None, want_logits=False, dX_out=None, loss_out=None, flags=0):
+    """Loss, dWa, dca, dX (and optionally the logits) of the auxiliary cluster head."""
+    import torch
+    lib = load()
+    _bf16_2d(X, "X")
+    _bf16_2d(Wa, "Wa")
+    B, d = X.shape
+    C = Wa.shape[1]
+    dev = X.device
+    s = 1.0 / B if s is None else s
+    loss = loss_out if loss_out is not None else torch.zeros(1, dtype=torch.float32, device=dev)
+    dWa = torch.empty((d, C), dtype=torch.float32, device=dev)
+    dca = torch.empty(C, dtype=torch.float32, device=dev) if ca is not None else None
+    dX = dX_out if dX_out is not None else torch.empty((B, d), dtype=torch.float32, device=dev)
+    Z = torch.empty((B, C), dtype=torch.float32, device=dev) if want_logits else None
+    ws_bytes = lib.ffsl_aux_workspace_bytes(B, d, C)
+    if ws_bytes == 0:
+        raise FfslError(FFSL_EINVAL, lib.ffsl_last_error().decode())
+    ws = _workspace(torch, ws_bytes, dev)
+    _check(lib.ffsl_aux_bce_fwd_bwd(_ptr(X), B, d, C, _ptr(Wa), _ptr(ca), _ptr(off), _ptr(lab), int(lab.numel()),
+                                    float(s), _ptr(loss), _ptr(dWa), _ptr(dca), _ptr(dX), _ptr(Z), flags,
+                                    _ptr(ws), ws.numel(), _stream(torch)))
+    return loss, dWa, dca, dX, Z
+
+
+def adam_dense(param, grad, m, v, t, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0):
+    """Adam / AdamW step in place on a flat (any-shape, contiguous) parameter tensor."""
+    import torch
+    lib = load()
+    if param.dtype == torch.bfloat16:
+        vt = FFSL_BF16
+    elif param.dtype == torch.float32:
+        vt = FFSL_F32
+    else:
+        raise TypeError("param must be float32 or bfloat16")
+    n = param.numel()
+    for name, x in (("grad", grad), ("m", m), ("v", v)):
+        if x.dtype != torch.float32 or x.numel() != n or not x.is_contiguous():
+            raise TypeError("%s must be a contiguous float32 tensor with %d elements" % (name, n))
+    _check(lib.ffsl_adam_dense(_ptr(param), vt, _ptr(grad), _ptr(m), _ptr(v), n, int(t), lr, beta1, beta2, eps,
+                               wd, _stream(torch)))
+
