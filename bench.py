@@ -99,6 +99,88 @@ def load_traffic(workload, src_hash):
     return t.get("bytes_per_launch")
 
 
+def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
+    """The dense intermediate layer (fwd + bwd) at the C3 shape and the
+    auxiliary head (fwd + bwd) at the C5 shape, each timed alone with HIP
+    events around the library calls (median of `reps`)."""
+    import numpy as np
+    lib = ffsl.load()
+    rng = np.random.default_rng(3)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def median_us(fn):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            a, b = ev.create(), ev.create()
+            ev.record(a, stream)
+            fn()
+            ev.record(b, stream)
+            torch.cuda.synchronize()
+            ms.append(ev.elapsed_ms(a, b))
+            ev.destroy(a)
+            ev.destroy(b)
+        return sorted(ms)[len(ms) // 2] * 1e3
+
+    out = {}
+    # intermediate layer, C3: X [128,768] -> H [128,2048]
+    w3 = synth.WORKLOADS["c3_inter2048_L1M"]
+    B, din, dout = w3.B, w3.din, w3.d
+    X = bf(synth.gen_x(rng, B, din, "layernorm", "bf16"))
+    W1 = bf(synth.make_dense(rng, din, dout))
+    c = torch.zeros(dout, device=dev)
+    A = torch.empty((B, dout), device=dev)
+    H = torch.empty((B, dout), dtype=torch.bfloat16, device=dev)
+    dH = torch.randn((B, dout), device=dev) * 1e-2
+    dW1 = torch.empty((din, dout), device=dev)
+    dc = torch.empty(dout, device=dev)
+    dX = torch.empty((B, din), device=dev)
+    ws = torch.empty(lib.ffsl_dense_workspace_bytes(B, din, dout), dtype=torch.uint8, device=dev)
+    p = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def dense_step():
+        ffsl._check(lib.ffsl_dense_gelu_fwd(p(X), B, din, dout, p(W1), p(c), p(A), p(H), stream))
+        ffsl._check(lib.ffsl_dense_gelu_bwd(p(X), B, din, dout, p(W1), p(A), p(dH), p(dW1), p(dc), p(dX), 0,
+                                            p(ws), ws.numel(), stream))
+    us = median_us(dense_step)
+    flops = 3 * 2.0 * B * din * dout
+    # W1 read twice, dW1 written, A written and read, H written, dH read, dA written and read
+    byts = 2 * din * dout * 2 + din * dout * 4 + B * dout * (4 + 4 + 2 + 4 + 2 + 2)
+    out["dense_gelu"] = {"shape": {"B": B, "din": din, "dout": dout}, "us_median": us,
+                         "flops": flops, "tflops": flops / (us * 1e-6) / 1e12, "mfma_peak_tflops": 2500.0,
+                         "algorithmic_bytes": byts, "gbs": byts / (us * 1e-6) / 1e9}
+    # auxiliary head, C5: X [128,768], C = 8192 clusters over L = 1M labels
+    w5 = synth.WORKLOADS["c5_aux8192_L1M"]
+    B, d, C = w5.B, w5.d, w5.aux_clusters
+    X5 = bf(synth.gen_x(rng, B, d, "layernorm", "bf16"))
+    Wa = bf(synth.make_dense(rng, d, C))
+    ca = torch.zeros(C, device=dev)
+    off, lab = synth.gen_targets(rng, B, w5.L, w5.mean_pos, w5.zipf_s)
+    offt = torch.from_numpy(off.astype(np.int32)).to(dev)
+    labt = torch.from_numpy(lab.astype(np.int32)).to(dev)
+    loss = torch.zeros(1, device=dev)
+    dWa = torch.empty((d, C), device=dev)
+    dca = torch.empty(C, device=dev)
+    dX5 = torch.empty((B, d), device=dev)
+    ws5 = torch.empty(lib.ffsl_aux_workspace_bytes(B, d, C), dtype=torch.uint8, device=dev)
+
+    def aux_step():
+        ffsl._check(lib.ffsl_aux_bce_fwd_bwd(p(X5), B, d, C, p(Wa), p(ca), p(offt), p(labt), len(lab),
+                                             1.0 / B, p(loss), p(dWa), p(dca), p(dX5), None, 0, p(ws5),
+                                             ws5.numel(), stream))
+    us = median_us(aux_step)
+    flops = 3 * 2.0 * B * d * C
+    # Wa read twice, dWa written, dZ written and read in fp32 and bf16
+    byts = 2 * d * C * 2 + d * C * 4 + B * C * (4 + 4 + 2 + 2 + 2)
+    out["aux_head"] = {"shape": {"B": B, "d": d, "C": C}, "us_median": us,
+                       "flops": flops, "tflops": flops / (us * 1e-6) / 1e12, "mfma_peak_tflops": 2500.0,
+                       "algorithmic_bytes": byts, "gbs": byts / (us * 1e-6) / 1e9}
+    return out
+
+
 def cpu_baseline(w, inp, target_s=12.0):
     """The oracle (float64, single thread) on the first L' label rows of the
     same workload: one fused step (forward, BCE, backward, Adam)."""
@@ -154,6 +236,7 @@ def main():
     ap.add_argument("--workload", default="c4_bf16_L3M")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--set-reps", type=int, default=10)
+    ap.add_argument("--dense-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
@@ -264,6 +347,10 @@ def main():
     print("[bench] SET: %.3f ms median, %.0f GB/s algorithmic, exhausted rows %d" %
           (set_ms_med, set_gbs, int(exhausted.cpu()[0])), file=sys.stderr, flush=True)
 
+    dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
+    print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
+          (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
@@ -309,6 +396,8 @@ def main():
             "frac": set_gbs / HBM_PEAK_GBS,
             "prune_per_row": n_set,
         },
+        "dense_gelu": dense["dense_gelu"],
+        "aux_head": dense["aux_head"],
         "cpu_baseline": cpu,
         "loss": final_loss,
     }

@@ -9,10 +9,12 @@
 //
 // bf16 operands, fp32 accumulation.  A workgroup of 256 threads computes a
 // 64 x 64 tile; each wave a 32 x 32 quarter with 2 x 2 v_mfma_f32_16x16x32_bf16
-// per 32-deep K step.  Both operands are staged into LDS K-contiguous, so
-// every fragment is one 16-byte LDS read whatever the source layout.  Long K
-// (the dX products) is split over blockIdx.z into fp32 partials that a second
-// kernel sums in a fixed order.
+// per 32-deep slice.  K advances 128 at a time: both operands are staged into
+// LDS K-contiguous (every fragment is one 16-byte LDS read whatever the source
+// layout), and the next 128-deep tiles are loaded into registers while the
+// matrix cores work on the current ones.  Long K (the dX products) is split
+// over blockIdx.z into fp32 partials that a second kernel sums in a fixed
+// order.
 #include <math.h>
 
 #include <algorithm>
@@ -27,7 +29,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int GT = 64;        // tile edge in M and N
-constexpr int GK = 32;        // K per stage
+constexpr int GK = 128;       // K per stage
 constexpr int GKP = GK + 8;   // LDS row in elements (padded against bank conflicts)
 
 enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2, EPI_BCE = 3 };
@@ -48,31 +50,51 @@ struct GemmArgs {
     float *loss_part;         // BCE: one partial per workgroup
 };
 
-// Stage a 64-row x 32-deep tile of one operand into S[row][k].
-//   KC = true : source stored row-major with k contiguous, src[r*ld + k]
-//   KC = false: source stored with the rows contiguous,   src[k*ld + r]
+// One operand's 64-row x 128-deep tile in flight: four 16-byte groups per
+// thread.
+struct Tile {
+    uint4 q[4];
+};
+
+// Load a tile of one operand into registers.
+//   KC = true : source stored row-major with k contiguous, src[r*ld + k];
+//               thread t takes row (t>>4) + 16 p, k group (t&15)*8
+//   KC = false: source stored with the rows contiguous,   src[k*ld + r];
+//               thread t takes k (t>>3) + 32 p, row group (t&7)*8
 // Out-of-range rows and k read as zero.  Callers guarantee that the contiguous
 // extent (K for KC, the row count otherwise) is a multiple of 8 and that
 // src and ld keep every 8-element group 16-byte aligned.
 template <bool KC>
-__device__ __forceinline__ void stage(uint16_t (*S)[GKP], const uint16_t *src, int64_t ld, int r0, int R,
-                                      int k0, int kend, int tid) {
-    if (KC) {
-        const int r = tid >> 2, kc = (tid & 3) * 8;
-        const int gr = r0 + r, gk = k0 + kc;
-        uint4 q = make_uint4(0u, 0u, 0u, 0u);
-        if (gr < R && gk < kend) q = *reinterpret_cast<const uint4 *>(src + (int64_t)gr * ld + gk);
-        *reinterpret_cast<uint4 *>(&S[r][kc]) = q;
-    } else {
-        const int kr = tid >> 3, rc = (tid & 7) * 8;
-        const int gk = k0 + kr, gr = r0 + rc;
-        uint4 q = make_uint4(0u, 0u, 0u, 0u);
-        if (gk < kend && gr < R) q = *reinterpret_cast<const uint4 *>(src + (int64_t)gk * ld + gr);
-        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+__device__ __forceinline__ void load_tile(Tile &t, const uint16_t *src, int64_t ld, int r0, int R, int k0,
+                                          int kend, int tid) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            S[rc + 2 * e][kr] = (uint16_t)(w[e] & 0xffffu);
-            S[rc + 2 * e + 1][kr] = (uint16_t)(w[e] >> 16);
+    for (int p = 0; p < 4; ++p) {
+        t.q[p] = make_uint4(0u, 0u, 0u, 0u);
+        if (KC) {
+            const int gr = r0 + (tid >> 4) + 16 * p, gk = k0 + (tid & 15) * 8;
+            if (gr < R && gk < kend) t.q[p] = *reinterpret_cast<const uint4 *>(src + (int64_t)gr * ld + gk);
+        } else {
+            const int gk = k0 + (tid >> 3) + 32 * p, gr = r0 + (tid & 7) * 8;
+            if (gk < kend && gr < R) t.q[p] = *reinterpret_cast<const uint4 *>(src + (int64_t)gk * ld + gr);
+        }
+    }
+}
+
+// Store a loaded tile into S[row][k] (K-contiguous).
+template <bool KC>
+__device__ __forceinline__ void store_tile(uint16_t (*S)[GKP], const Tile &t, int tid) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        if (KC) {
+            *reinterpret_cast<uint4 *>(&S[(tid >> 4) + 16 * p][(tid & 15) * 8]) = t.q[p];
+        } else {
+            const int kr = (tid >> 3) + 32 * p, rc = (tid & 7) * 8;
+            const uint32_t w[4] = {t.q[p].x, t.q[p].y, t.q[p].z, t.q[p].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                S[rc + 2 * e][kr] = (uint16_t)(w[e] & 0xffffu);
+                S[rc + 2 * e + 1][kr] = (uint16_t)(w[e] >> 16);
+            }
         }
     }
 }
@@ -94,22 +116,33 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    Tile ta, tb;
+    load_tile<!TA>(ta, g.A, g.lda, m0, g.M, kbeg, kend, tid);
+    load_tile<TB>(tb, g.B, g.ldb, n0, g.N, kbeg, kend, tid);
     for (int k0 = kbeg; k0 < kend; k0 += GK) {
-        stage<!TA>(As, g.A, g.lda, m0, g.M, k0, kend, tid);
-        stage<TB>(Bs, g.B, g.ldb, n0, g.N, k0, kend, tid);
+        store_tile<!TA>(As, ta, tid);
+        store_tile<TB>(Bs, tb, tid);
         __syncthreads();
-        bf16x8 af[2], bv[2];
+        if (k0 + GK < kend) {   // the next tiles load while this one computes
+            load_tile<!TA>(ta, g.A, g.lda, m0, g.M, k0 + GK, kend, tid);
+            load_tile<TB>(tb, g.B, g.ldb, n0, g.N, k0 + GK, kend, tid);
+        }
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-            af[mi] = *reinterpret_cast<const bf16x8 *>(&As[32 * wm + 16 * mi + col][8 * kq]);
+        for (int ks = 0; ks < GK; ks += 32) {
+            bf16x8 af[2], bv[2];
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-            bv[ni] = *reinterpret_cast<const bf16x8 *>(&Bs[32 * wn + 16 * ni + col][8 * kq]);
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
+            for (int mi = 0; mi < 2; ++mi)
+                af[mi] = *reinterpret_cast<const bf16x8 *>(&As[32 * wm + 16 * mi + col][ks + 8 * kq]);
 #pragma unroll
             for (int ni = 0; ni < 2; ++ni)
-                acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mi], bv[ni], acc[mi][ni], 0, 0, 0);
+                bv[ni] = *reinterpret_cast<const bf16x8 *>(&Bs[32 * wn + 16 * ni + col][ks + 8 * kq]);
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 2; ++ni)
+                    acc[mi][ni] =
+                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mi], bv[ni], acc[mi][ni], 0, 0, 0);
+        }
         __syncthreads();
     }
 
@@ -156,36 +189,55 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
     }
 }
 
+// Column kernels: a workgroup owns 32 columns; its 8 row groups take every
+// 8th row and a fixed tree in LDS adds the groups' sums.
+__device__ __forceinline__ void column_sum_out(float (*red)[33], float sum, int c, int rg, int n, int N,
+                                               float *out) {
+    red[rg][c] = sum;
+    __syncthreads();
+    if (rg == 0 && n < N && out) {
+        float t = red[0][c];
+        for (int g = 1; g < 8; ++g) t += red[g][c];
+        out[n] = t;
+    }
+}
+
 // dA = dH * GELU'(A), GELU'(a) = Phi(a) + a phi(a); the bf16 copy feeds the
-// two products, the fp32 column sums are dc.  One thread per column.
+// two products, the fp32 column sums are dc.
 __global__ void __launch_bounds__(256) k_gelu_bwd_cols(const float *A, const float *dH, int B, int N,
                                                        uint16_t *dA16, float *dc) {
-    const int n = blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
+    __shared__ float red[8][33];
+    const int c = threadIdx.x & 31, rg = threadIdx.x >> 5;
+    const int n = blockIdx.x * 32 + c;
     float sum = 0.f;
-    for (int b = 0; b < B; ++b) {
-        const int64_t o = (int64_t)b * N + n;
-        const float a = A[o];
-        const float pdf = 0.39894228040143268f * expf(-0.5f * a * a);
-        const float da = dH[o] * (gelu_cdf(a) + a * pdf);
-        dA16[o] = f32_to_bf16_bits(da);
-        sum += da;
+    if (n < N) {
+        for (int b = rg; b < B; b += 8) {
+            const int64_t o = (int64_t)b * N + n;
+            const float a = A[o];
+            const float pdf = 0.39894228040143268f * expf(-0.5f * a * a);
+            const float da = dH[o] * (gelu_cdf(a) + a * pdf);
+            dA16[o] = f32_to_bf16_bits(da);
+            sum += da;
+        }
     }
-    if (dc) dc[n] = sum;
+    column_sum_out(red, sum, c, rg, n, N, dc);
 }
 
 // column sums of an fp32 [B,N] matrix (nullable) and its bf16 copy
 __global__ void __launch_bounds__(256) k_cols_cvt(const float *Z, int B, int N, uint16_t *Z16, float *csum) {
-    const int n = blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
+    __shared__ float red[8][33];
+    const int c = threadIdx.x & 31, rg = threadIdx.x >> 5;
+    const int n = blockIdx.x * 32 + c;
     float sum = 0.f;
-    for (int b = 0; b < B; ++b) {
-        const int64_t o = (int64_t)b * N + n;
-        const float z = Z[o];
-        Z16[o] = f32_to_bf16_bits(z);
-        sum += z;
+    if (n < N) {
+        for (int b = rg; b < B; b += 8) {
+            const int64_t o = (int64_t)b * N + n;
+            const float z = Z[o];
+            Z16[o] = f32_to_bf16_bits(z);
+            sum += z;
+        }
     }
-    if (csum) csum[n] = sum;
+    column_sum_out(red, sum, c, rg, n, N, csum);
 }
 
 // out[e] (+)= sum_z P[z][e], the split-K partials in ascending z
@@ -313,7 +365,7 @@ int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uin
                           hipStream_t st) {
     const DenseWs w = dense_ws(B, din, dout);
     uint16_t *dA16 = reinterpret_cast<uint16_t *>(ws + w.dA16);
-    hipLaunchKernelGGL(k_gelu_bwd_cols, dim3((dout + 255) / 256), dim3(256), 0, st, A, dH, B, dout, dA16, dc);
+    hipLaunchKernelGGL(k_gelu_bwd_cols, dim3((dout + 31) / 32), dim3(256), 0, st, A, dH, B, dout, dA16, dc);
     int rc = check_launch("gelu_bwd_cols");
     if (rc) return rc;
     // dW1[i,o] = sum_b X[b,i] dA[b,o]: A(m=i, k=b) = X[b*din+i] (TA), B(k=b, n=o) = dA[b*dout+o]
@@ -394,7 +446,7 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, c
         rc = check_launch("sum_partials");
         if (rc) return rc;
     }
-    hipLaunchKernelGGL(k_cols_cvt, dim3((C + 255) / 256), dim3(256), 0, st, dz, B, C, dz16, dca);
+    hipLaunchKernelGGL(k_cols_cvt, dim3((C + 31) / 32), dim3(256), 0, st, dz, B, C, dz16, dca);
     rc = check_launch("cols_cvt");
     if (rc) return rc;
     // dWa[i,c] = sum_b X[b,i] dZ[b,c]

@@ -299,6 +299,45 @@ __global__ void k_dx_reduce(const float *part, int nparts, int64_t n, float *out
     }
 }
 
+// The same sum for n divisible by 4: a workgroup owns 64 consecutive
+// elements (16 float4 columns); its 16 lane groups take every 16th partial
+// with independent 16-byte loads, and a fixed tree in LDS adds the groups.
+__global__ void __launch_bounds__(256) k_dx_reduce4(const float4 *part, int nparts, int64_t n4, float4 *out,
+                                                    int accum) {
+    __shared__ float4 red[16][16];
+    const int eg = threadIdx.x & 15, pg = threadIdx.x >> 4;
+    const int64_t e = (int64_t)blockIdx.x * 16 + eg;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (e < n4) {
+        for (int p = pg; p < nparts; p += 16) {
+            const float4 q = part[(size_t)p * n4 + e];
+            s.x += q.x;
+            s.y += q.y;
+            s.z += q.z;
+            s.w += q.w;
+        }
+    }
+    red[pg][eg] = s;
+    __syncthreads();
+    if (pg == 0 && e < n4) {
+        float4 t = red[0][eg];
+        for (int g = 1; g < 16; ++g) {
+            t.x += red[g][eg].x;
+            t.y += red[g][eg].y;
+            t.z += red[g][eg].z;
+            t.w += red[g][eg].w;
+        }
+        if (accum) {
+            const float4 o = out[e];
+            t.x += o.x;
+            t.y += o.y;
+            t.z += o.z;
+            t.w += o.w;
+        }
+        out[e] = t;
+    }
+}
+
 // loss (+)= s * sum of workgroup partials, fixed order
 __global__ void k_loss_reduce(const float *part, int nparts, float s, float *out, int accum) {
     __shared__ float red[256];
@@ -429,9 +468,17 @@ int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_par
     }
     if (c.mode != SWEEP_FWD && c.dX_out) {
         const int64_t n = (int64_t)B * d;
-        const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
-        hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, grid, n, c.dX_out,
-                           (c.flags & FFSL_ACCUM_DX) ? 1 : 0);
+        const int accum = (c.flags & FFSL_ACCUM_DX) ? 1 : 0;
+        if (n % 4 == 0 && (reinterpret_cast<uintptr_t>(c.dX_out) & 15u) == 0) {
+            const int64_t n4 = n / 4;
+            hipLaunchKernelGGL(k_dx_reduce4, dim3((unsigned)((n4 + 15) / 16)), dim3(256), 0, c.stream,
+                               reinterpret_cast<const float4 *>(dx_part), grid, n4,
+                               reinterpret_cast<float4 *>(c.dX_out), accum);
+        } else {
+            const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
+            hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, grid, n, c.dX_out,
+                               accum);
+        }
         rc = check_launch("dx_reduce");
         if (rc) return rc;
     }
