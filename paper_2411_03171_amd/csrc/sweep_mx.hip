@@ -13,8 +13,9 @@
 //        G  [64][32] bf16  the chunk's dlogits
 //        Is, Ws            the chunk's index rows (as byte offsets into Xs)
 //                          and weight rows
-//        ym [32][2] u32    the chunk's targets as one 64-bit sample mask per row
-//        tg                the batch's positive (label, sample) pairs
+//        tg                the batch's positives as sorted (label, sample) keys;
+//                          with more positives than fit, ym [32][2] u32 (in the
+//                          same place) holds the chunk's targets built by a scan
 //
 //   1. gather: for each slot, lane u reads the 8 bytes X[4u..4u+3, I[l,j]]
 //      (16 lanes read one whole column, four columns per wave instruction,
@@ -24,9 +25,12 @@
 //   3. BCE loss and dlogits g for the lane's 4 batch rows;
 //   4. dW partials over the lane's 4 rows with v_dot2 (g rounded to bf16),
 //      then a reduce-scatter over the 16 lanes with DPP-fused adds.  Lane u
-//      keeps slot r XOR K(u) in register r, K(u) = 2u0^6u1^12u2^24u3, which
-//      makes every butterfly level one add with a mirror-pattern DPP source;
-//      lane u ends with the full dW of slots K(u), K(u)+1;
+//      keeps slot r XOR Kp(u) in register r, Kp(u) = (2u0^6u1^12u2^24u3) with
+//      bit 1 cleared, which makes the first three butterfly levels one add
+//      each with a mirror-pattern DPP source and lets the lane read its row's
+//      indices four at a time; at the last level lanes u and u^1 hold the
+//      same four slots, both add, and each keeps two: lane u ends with the
+//      full dW of slots Kp(u) + 2u0 and the next one;
 //   5. Adam on those two slots, streaming W, m, v back to HBM;
 //   6. dX: g and the old weights go to G and T, and the matrix cores add
 //      G x T^T (64 x 32 by 32 x d) into a per-workgroup dX held in AGPRs for
@@ -109,6 +113,13 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
                                            false);
 }
 
+// a.b with no accumulator (the three-operand form takes an inline zero)
+__device__ __forceinline__ float dot2z(uint32_t a, uint32_t b) {
+    float r;
+    asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     bf16x2 p = {(__bf16)lo, (__bf16)hi};
     return __builtin_bit_cast(uint32_t, p);
@@ -141,14 +152,16 @@ __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &v
 }
 
 struct Prefetch {
-    uint2 iv;                        // two index words of the chunk's I rows
-    uint32_t wv;                     // one weight word of the chunk's W rows
+    uint2 iv;          // two index words of the chunk's I rows
+    uint32_t wv;       // one weight word of the chunk's W rows
+    float2 m, v;       // moments of the lane's two slots (slot, slot + 1) of its row
+    float b;           // its bias
 };
 
 // the chunk's rows and optimiser state, loaded a chunk ahead of their use; a
 // chunk or row past the end reads zeros
 __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_t chunk, int tid, int lab, int u,
-                                         int K, Prefetch &p) {
+                                         int slot, Prefetch &p) {
     const int64_t l0 = chunk * MX_NLAB;
     const bool live = chunk < a.nchunks;
     const uint32_t oi = live ? (uint32_t)(l0 * MX_K * 4) + 8u * tid : a.nb_I;
@@ -156,8 +169,13 @@ __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_
     p.iv = make_uint2(iv[0], iv[1]);
     const uint32_t ow = live ? (uint32_t)(l0 * MX_K * 2) + 4u * tid : a.nb_W;
     p.wv = ld32(R.W, ow);
+    const int64_t l = l0 + lab;
+    const bool ok = live && l < a.L;
+    const uint32_t om = ok ? (uint32_t)(l * MX_K + slot) * 4u : a.nb_m;
+    p.m = ldf2(R.m, om);
+    p.v = ldf2(R.v, om);
+    p.b = ldf(R.b, ok ? (uint32_t)l * 4u : a.nb_b);
 }
-
 
 // NT = column tiles of 16 per wave: d = 128 * NT (a compile-time width keeps
 // the dX accumulators in fixed registers)
@@ -170,14 +188,19 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     uint16_t *G = T + (size_t)d * MX_NLAB;                                  // 64 * 32
     int32_t *Is = reinterpret_cast<int32_t *>(G + MX_NB * MX_NLAB);        // 32 * 32
     uint32_t *Ws = reinterpret_cast<uint32_t *>(Is + MX_NLAB * MX_K);      // 32 * 16
-    uint32_t *ym = Ws + MX_NLAB * (MX_K / 2);                              // 32 * 2
-    uint32_t *tg = ym + MX_NLAB * 2;                                       // MX_TG_MAX
+    uint32_t *tg = Ws + MX_NLAB * (MX_K / 2);                              // MX_TG_MAX
+    uint32_t *ym = tg;   // [32][2]: only when the positives do not fit in tg
 
     const int tid = threadIdx.x;
     const int lab = tid >> 4, u = tid & 15;
     const int wave = tid >> 6, lane = tid & 63;
-    const int K = lane_key(u);
-    const bool tg_lds = a.nnz <= MX_TG_MAX;
+    // register r of a lane holds slot r ^ Kp; Kp = lane_key with bit 1 cleared,
+    // so the lane reads its row's slots four at a time (two pairs).  The lane
+    // ends the dW reduce-scatter with the slots Kown, Kown + 1.
+    const int Kp = lane_key(u) & ~2;
+    const int Kown = Kp + 2 * (u & 1);
+    const int nnz = a.nnz;
+    const bool tg_lds = nnz <= MX_TG_MAX;
 
     Rsrcs R;
     R.X = make_rsrc(a.X, a.nb_X);
@@ -189,10 +212,10 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     R.bm = make_rsrc(a.bm, a.nb_b);
     R.bv = make_rsrc(a.bv, a.nb_b);
 
-    Prefetch cur, nxt;
-    prefetch(a, R, blockIdx.x, tid, lab, u, K, cur);
+    Prefetch pa, pb;
+    prefetch(a, R, blockIdx.x, tid, lab, u, Kown, pa);
 
-    // stage X transposed (b fastest) and zero past B; clear T; keep the positives
+    // stage X transposed (b fastest) and zero past B; clear T
     {
         // lane = sample, each wave takes groups of 8 columns: 16-byte row loads,
         // conflict-free 2-byte LDS stores
@@ -210,9 +233,39 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             }
         }
         for (int e = tid; e < d * MX_NLAB / 2; e += MX_THREADS) reinterpret_cast<uint32_t *>(T)[e] = 0u;
-        if (tg_lds)
-            for (int e = tid; e < a.nnz; e += MX_THREADS)
-                tg[e] = ((uint32_t)a.tgt_lab[e] << 6) | ((uint32_t)a.tgt_b[e] & 63u);
+    }
+    // The batch's positives as keys (label << 6 | sample), sorted ascending
+    // (bitonic sort in LDS; a label outside [0,L) becomes the largest key and
+    // is never matched).  Chunks of one workgroup come in ascending order, so
+    // a cursor that only moves forward finds each chunk's positives.
+    if (tg_lds) {
+        int n2 = 1;
+        while (n2 < nnz) n2 <<= 1;
+        for (int e = tid; e < n2; e += MX_THREADS) {
+            uint32_t key = 0xffffffffu;
+            if (e < nnz) {
+                const int32_t lb = a.tgt_lab[e];
+                const int32_t sb = a.tgt_b[e];
+                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < MX_NB) key = ((uint32_t)lb << 6) | (uint32_t)sb;
+            }
+            tg[e] = key;
+        }
+        __syncthreads();
+        for (int k = 2; k <= n2; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int i = tid; i < n2; i += MX_THREADS) {
+                    const int ij = i ^ j;
+                    if (ij > i) {
+                        const uint32_t x = tg[i], y = tg[ij];
+                        if (((i & k) == 0) ? (x > y) : (x < y)) {
+                            tg[i] = y;
+                            tg[ij] = x;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
     }
 
     // dX accumulators: 4 batch tiles x NT column tiles of 16 per wave (8 waves)
@@ -227,74 +280,95 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     const float decay = 1.f - a.adam.lr * a.adam.wd;
     const float inv_bc1 = 1.f / a.adam.bc1, inv_bc2 = 1.f / a.adam.bc2;
     const float b1 = a.adam.b1, b2 = a.adam.b2, lr = a.adam.lr, eps = a.adam.eps;
+    int pos = 0;              // first sorted key not below the current chunk
+    uint32_t head = 0xffffffffu;   // tg[pos] (uniform), or the largest key past the end
+    if (tg_lds && nnz > 0) head = tg[0];
+    int32_t c0 = 0, c1 = 0;   // T columns written by this lane in the previous chunk
 
-    for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += gridDim.x) {
+    // One chunk: `cur` holds its rows and optimiser state, `nxt` receives the
+    // next chunk's.
+    auto step = [&](int64_t chunk, const Prefetch &cur, Prefetch &nxt) {
         const int64_t l0 = chunk * MX_NLAB;
+        const uint32_t l0u = (uint32_t)l0;   // L < 2^25: label offsets fit in 32 bits
 
-        // stage this chunk's rows (loaded during the previous chunk): indices
-        // become clamped byte offsets of X columns
+        // stage this chunk's rows: indices become clamped byte offsets of X columns
         {
             const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
             *reinterpret_cast<int2 *>(Is + 2 * tid) = make_int2(i0 * MX_XS, i1 * MX_XS);
             Ws[tid] = cur.wv;
-            if (tid < MX_NLAB * 2) ym[tid] = 0u;
+            if (!tg_lds && tid < MX_NLAB * 2) ym[tid] = 0u;
         }
-        prefetch(a, R, chunk + gridDim.x, tid, lab, u, K, nxt);
+        prefetch(a, R, chunk + gridDim.x, tid, lab, u, Kown, nxt);
         __syncthreads();
-        {
-            // label offsets in 32 bits: a label before the chunk wraps to a large value
-            const uint32_t l0u = (uint32_t)l0;
-            if (tg_lds) {
-                for (int e = tid; e < a.nnz; e += MX_THREADS) {
+        // Every wave has read the previous chunk's G and T fragments before the
+        // barrier above, so this lane's T entries of that chunk can be cleared;
+        // the entries of one row are only ever touched by the wave that owns
+        // the row, in program order.
+        T[(size_t)c0 * MX_NLAB + lab] = 0;
+        T[(size_t)c1 * MX_NLAB + lab] = 0;
+
+        // targets of this lane's row as a 64-bit sample mask
+        uint64_t yrow = 0;
+        if (tg_lds) {
+            // a chunk without positives costs one compare of the cached head key;
+            // the cursor only moves past keys of chunks already behind
+            while ((head >> 6) < l0u) {
+                ++pos;
+                head = pos < nnz ? tg[pos] : 0xffffffffu;
+            }
+            if ((head >> 6) - l0u < (uint32_t)MX_NLAB) {
+                for (int e = pos; e < nnz; ++e) {
                     const uint32_t key = tg[e];
                     const uint32_t ll = (key >> 6) - l0u;
-                    if (ll < MX_NLAB) atomicOr(&ym[ll * 2 + ((key >> 5) & 1)], 1u << (key & 31));
-                }
-            } else {
-                for (int e = tid; e < a.nnz; e += MX_THREADS) {
-                    const uint32_t ll = (uint32_t)a.tgt_lab[e] - l0u;
-                    const uint32_t b = (uint32_t)a.tgt_b[e];
-                    if (ll < MX_NLAB && b < MX_NB) atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
+                    if (ll >= (uint32_t)MX_NLAB) break;
+                    if (ll == (uint32_t)lab) yrow |= 1ull << (key & 63u);
                 }
             }
+        } else {
+            for (int e = tid; e < nnz; e += MX_THREADS) {
+                const uint32_t ll = (uint32_t)a.tgt_lab[e] - l0u;
+                const uint32_t b = (uint32_t)a.tgt_b[e];
+                if (ll < MX_NLAB && b < MX_NB) atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
+            }
+            __syncthreads();
+            yrow = (uint64_t)ym[lab * 2] | ((uint64_t)ym[lab * 2 + 1] << 32);
         }
-        __syncthreads();
 
-        int32_t c0 = 0, c1 = 0;   // columns of slots K, K+1: cleared in T after the dX step
         {
             int rl = lab;            // the row of the chunk this lane serves
-            int k2 = K >> 1;         // pair order of this lane
+            int k4 = Kp >> 2;        // quad order of this lane
             // opaque per chunk, so the per-slot LDS addresses are formed where
             // they are used instead of being held in registers across chunks
-            asm volatile("" : "+v"(rl), "+v"(k2));
+            asm volatile("" : "+v"(rl), "+v"(k4));
             const int64_t l = l0 + rl;
             const bool valid = l < a.L;
-            // optimiser state of slots K, K+1 and of the bias (zeros past L)
-            const uint32_t om = valid ? (uint32_t)(l * MX_K + K) * 4u : a.nb_m;
-            const float2 mcur = ldf2(R.m, om);
-            const float2 vcur = ldf2(R.v, om);
-            const uint32_t obl = valid ? (uint32_t)l * 4u : a.nb_b;
-            const float bcur = ldf(R.b, obl);
-            const float bmcur = ldf(R.bm, u == 0 ? obl : a.nb_b);
-            const float bvcur = ldf(R.bv, u == 0 ? obl : a.nb_b);
+            // the bias moments, used on lane u = 0 at the end of the row's work
+            const uint32_t obm = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
+            const float bmcur = ldf(R.bm, obm), bvcur = ldf(R.bv, obm);
 
             // row data in the lane's slot order: register r <-> slot r ^ K (a row
             // past L has zero offsets and weights)
             uint32_t wp[MX_K / 2];
             uint2 xg[MX_K];
+            const bool odd = (u & 1) != 0;
+            uint32_t wpair_own = 0u;
 #pragma unroll
-            for (int p = 0; p < MX_K / 2; ++p) {
-                const int pp = p ^ k2;
-                const int2 iv = *reinterpret_cast<const int2 *>(Is + rl * MX_K + 2 * pp);
-                if (p == 0) {
-                    c0 = iv.x / MX_XS;
-                    c1 = iv.y / MX_XS;
+            for (int q = 0; q < MX_K / 4; ++q) {
+                const int qq = q ^ k4;   // registers 4q..4q+3 hold slots 4qq..4qq+3
+                const int4 iv = *reinterpret_cast<const int4 *>(Is + rl * MX_K + 4 * qq);
+                const uint2 wv = *reinterpret_cast<const uint2 *>(Ws + rl * (MX_K / 2) + 2 * qq);
+                if (q == 0) {   // the lane's own slots are registers 2*odd, 2*odd + 1
+                    c0 = (odd ? iv.z : iv.x) / MX_XS;
+                    c1 = (odd ? iv.w : iv.y) / MX_XS;
+                    wpair_own = odd ? wv.y : wv.x;
                 }
-                xg[2 * p] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
-                xg[2 * p + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
-                wp[p] = Ws[rl * (MX_K / 2) + pp];
+                xg[4 * q] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
+                xg[4 * q + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
+                xg[4 * q + 2] = *reinterpret_cast<const uint2 *>(Xs + iv.z + 8 * u);
+                xg[4 * q + 3] = *reinterpret_cast<const uint2 *>(Xs + iv.w + 8 * u);
+                wp[2 * q] = wv.x;
+                wp[2 * q + 1] = wv.y;
             }
-            const uint32_t wpair_own = wp[0];
             // forward: repack (b, b+1) pairs of two slots into slot pairs
             float z[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -307,12 +381,12 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             }
             // BCE and dlogits for rows 4u..4u+3; zero for padded samples and
             // rows past L
-            const uint32_t yw = ym[rl * 2 + (u >> 3)] >> ((4 * u) & 31);
+            const uint32_t yw = (uint32_t)(yrow >> (4 * u));
             float g[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const bool live = valid && 4 * u + e < a.B;
-                const float zz = z[e] + bcur;
+                const float zz = z[e] + cur.b;
                 const float y = ((yw >> e) & 1u) ? 1.f : 0.f;
                 const float ex = __expf(-fabsf(zz));
                 const float opx = 1.f + ex;
@@ -321,11 +395,11 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __logf(opx) : 0.f;
                 g[e] = live ? a.s * (sig - y) : 0.f;
             }
-            // dW partials over the lane's rows, slot order r ^ K
+            // dW partials over the lane's rows, slot order r ^ Kp
             const uint32_t g01 = pack_bf16(g[0], g[1]), g23 = pack_bf16(g[2], g[3]);
             float pw[MX_K];
 #pragma unroll
-            for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2(xg[r].x, g01, 0.f));
+            for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2z(xg[r].x, g01));
             // reduce-scatter over the 16 lanes of the row
 #pragma unroll
             for (int r = 0; r < 16; ++r) pw[r] = add_dpp<DPP_ROW_MIRROR>(pw[r], pw[16 + r]);
@@ -333,16 +407,19 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             for (int r = 0; r < 8; ++r) pw[r] = add_dpp<DPP_ROW_HALF_MIRROR>(pw[r], pw[8 + r]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_3210>(pw[r], pw[4 + r]);
+            // last level: lanes u and u^1 hold the same four slots; both add, each
+            // keeps its two
 #pragma unroll
-            for (int r = 0; r < 2; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[2 + r]);
-            // Adam on slots K, K+1
+            for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[r]);
+            const float dw0 = odd ? pw[2] : pw[0], dw1 = odd ? pw[3] : pw[1];
+            // Adam on slots Kown, Kown+1
             {
-                float m0 = mcur.x, m1 = mcur.y, v0 = vcur.x, v1 = vcur.y;
+                float m0 = cur.m.x, m1 = cur.m.y, v0 = cur.v.x, v1 = cur.v.y;
                 const float w0 = __uint_as_float(wpair_own << 16);
                 const float w1 = __uint_as_float(wpair_own & 0xffff0000u);
-                const float n0 = adam_step(w0, pw[0], m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                const float n1 = adam_step(w1, pw[1], m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                const uint32_t o = (uint32_t)(l * MX_K + K);
+                const float n0 = adam_step(w0, dw0, m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                const float n1 = adam_step(w1, dw1, m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                const uint32_t o = (uint32_t)(l * MX_K + Kown);
                 stf2(R.m, valid ? 4u * o : a.nb_m, make_float2(m0, m1));
                 stf2(R.v, valid ? 4u * o : a.nb_m, make_float2(v0, v1));
                 st32(R.W, valid ? 2u * o : a.nb_W, pack_bf16(n0, n1));
@@ -355,11 +432,10 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 sg = add_dpp<DPP_QUAD_3210>(sg, sg);
                 sg = add_dpp<DPP_QUAD_1032>(sg, sg);
                 float mm = bmcur, vv = bvcur;
-                const float nb = adam_step(bcur, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                const uint32_t ob = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
-                stf(R.b, ob, nb);
-                stf(R.bm, ob, mm);
-                stf(R.bv, ob, vv);
+                const float nb = adam_step(cur.b, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                stf(R.b, obm, nb);
+                stf(R.bm, obm, mm);
+                stf(R.bv, obm, vv);
             }
             // dX inputs: g and the old weights (a row past L writes zeros at column 0)
 #pragma unroll
@@ -370,8 +446,9 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         }
         __syncthreads();
         // dX += G (64 x 32) * T^T (32 x d) on the matrix cores; this wave owns
-        // columns [wave*d/8, (wave+1)*d/8).  The fragment reads finish before
-        // the barrier below; the MFMAs run on while the next chunk starts.
+        // columns [wave*d/8, (wave+1)*d/8).  The MFMAs run on while the next
+        // chunk starts; its first barrier orders the fragment reads before any
+        // rewrite of G or T.
         {
             const int col = lane & 15, kq = lane >> 4;
             bf16x8 af[4];
@@ -389,10 +466,14 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 for (int mt = 0; mt < 4; ++mt)
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mt], bfr[nt], acc[mt][nt], 0, 0, 0);
         }
-        __syncthreads();
-        T[(size_t)c0 * MX_NLAB + lab] = 0;
-        T[(size_t)c1 * MX_NLAB + lab] = 0;
-        cur = nxt;
+    };
+
+    // two chunks per iteration, so the prefetch buffers swap roles instead of
+    // being copied (a copy would wait for the loads in flight)
+    for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += 2 * (int64_t)gridDim.x) {
+        step(chunk, pa, pb);
+        if (chunk + gridDim.x >= a.nchunks) break;
+        step(chunk + gridDim.x, pb, pa);
     }
 
     // write this workgroup's dX partial [B][d]
@@ -434,7 +515,7 @@ const MxKernel *mx_kernels() {
 
 size_t sweep_mx_lds(int d) {
     return (size_t)d * MX_XS + (size_t)d * MX_NLAB * 2 + MX_NB * MX_NLAB * 2 + MX_NLAB * MX_K * 4 +
-           MX_NLAB * (MX_K / 2) * 4 + MX_NLAB * 2 * 4 + MX_TG_MAX * 4;
+           MX_NLAB * (MX_K / 2) * 4 + MX_TG_MAX * 4;
 }
 
 }  // namespace
