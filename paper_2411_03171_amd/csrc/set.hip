@@ -17,6 +17,8 @@
 //     bitmap bit is clear and then marking it;
 //   - writes the accepted columns to the pruned slots in ascending slot
 //     order, with W = +0 and m = v = 0; all other slots are left untouched.
+#include <type_traits>
+
 #include "ffsl_internal.h"
 
 namespace ffsl {
@@ -150,12 +152,45 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
         }
     }
 
-    // n smallest (key, slot): pass s finds the smallest pair strictly above
-    // the pair found by pass s-1.
+    uint64_t pruned_lo = 0, pruned_hi = 0;  // slot bitmask, KM <= 128
+    if (n <= 4) {
+        // the n smallest of the unique keys (|W| bits, slot) held in sorted
+        // order by an insertion network of depth 4 over all k slots
+        // bf16 keys (15 bits) and the slot fit one 32-bit word
+        using KeyT = typename std::conditional<VT == FFSL_BF16, uint32_t, uint64_t>::type;
+        const KeyT top = (KeyT)~(KeyT)0;
+        KeyT s0 = top, s1 = top, s2 = top, s3 = top;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+            if (j < k) {
+                KeyT x = ((KeyT)key[j] << 7) | (KeyT)j;
+                KeyT t = min(s0, x);
+                x = max(s0, x);
+                s0 = t;
+                t = min(s1, x);
+                x = max(s1, x);
+                s1 = t;
+                t = min(s2, x);
+                x = max(s2, x);
+                s2 = t;
+                s3 = min(s3, x);
+            }
+        }
+        const KeyT sel[4] = {s0, s1, s2, s3};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (q < n) {
+                const int bj = (int)(sel[q] & 127u);
+                if (bj < 64) pruned_lo |= 1ull << bj;
+                else pruned_hi |= 1ull << (bj - 64);
+            }
+        }
+    }
+    // n > 4: pass s finds the smallest pair strictly above the pair found by
+    // pass s-1.
     uint32_t pk = 0;
     int pj = -1;
-    uint64_t pruned_lo = 0, pruned_hi = 0;  // slot bitmask, KM <= 128
-    for (int s = 0; s < n; ++s) {
+    for (int s = 0; s < (n <= 4 ? 0 : n); ++s) {
         uint32_t bk = 0xffffffffu;
         int bj = KM;
 #pragma unroll
