@@ -10,7 +10,8 @@
 //   LDS  Xs [d][64] bf16   the batch transposed (column i is 128 contiguous
 //                          bytes), zero-padded past B
 //        T  [d][32] bf16   the chunk's weights scattered densely by column
-//        G  [64][32] bf16  the chunk's dlogits
+//        G  [64][32] bf16  the chunk's dlogits (both with XOR-swizzled 16-byte
+//                          chunks, see swz)
 //        Is, Ws            the chunk's index rows (as byte offsets into Xs)
 //                          and weight rows
 //        tg                the batch's positives as sorted (label, sample) keys;
@@ -136,6 +137,14 @@ constexpr int DPP_ROW_MIRROR = 0x140;       // lane j <- 15 - j within 16
 constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane j <- 7 - j within 8
 constexpr int DPP_QUAD_3210 = 0x1B;         // lane j <- j ^ 3 within 4
 constexpr int DPP_QUAD_1032 = 0xB1;         // lane j <- j ^ 1 within 4
+
+// G and T rows hold 32 bf16 (64 bytes = four 16-byte chunks).  The matrix-
+// core fragments read one chunk from each of 16 consecutive rows; stored
+// plainly, rows r and r+4 would hit the same banks.  Chunk q of row r is
+// therefore kept at chunk q ^ ((r >> 2) & 3); element e of row r sits at:
+__device__ __forceinline__ int swz(int r, int e) {
+    return r * MX_NLAB + ((((e >> 3) ^ (r >> 2)) & 3) << 3) + (e & 7);
+}
 
 __device__ __forceinline__ int lane_key(int u) {
     return ((u & 1) ? 2 : 0) ^ ((u & 2) ? 6 : 0) ^ ((u & 4) ? 12 : 0) ^ ((u & 8) ? 24 : 0);
@@ -304,8 +313,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         // barrier above, so this lane's T entries of that chunk can be cleared;
         // the entries of one row are only ever touched by the wave that owns
         // the row, in program order.
-        T[(size_t)c0 * MX_NLAB + lab] = 0;
-        T[(size_t)c1 * MX_NLAB + lab] = 0;
+        T[swz(c0, lab)] = 0;
+        T[swz(c1, lab)] = 0;
 
         // targets of this lane's row as a 64-bit sample mask
         uint64_t yrow = 0;
@@ -440,9 +449,9 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             // dX inputs: g and the old weights (a row past L writes zeros at column 0)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                G[(4 * u + e) * MX_NLAB + rl] = (uint16_t)((e < 2 ? g01 : g23) >> (16 * (e & 1)));
-            T[(size_t)c0 * MX_NLAB + rl] = (uint16_t)(wpair_own & 0xffffu);
-            T[(size_t)c1 * MX_NLAB + rl] = (uint16_t)(wpair_own >> 16);
+                G[swz(4 * u + e, rl)] = (uint16_t)((e < 2 ? g01 : g23) >> (16 * (e & 1)));
+            T[swz(c0, rl)] = (uint16_t)(wpair_own & 0xffffu);
+            T[swz(c1, rl)] = (uint16_t)(wpair_own >> 16);
         }
         __syncthreads();
         // dX += G (64 x 32) * T^T (32 x d) on the matrix cores; this wave owns
@@ -454,12 +463,11 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             bf16x8 af[4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
-                af[mt] = *reinterpret_cast<const bf16x8 *>(G + (16 * mt + col) * MX_NLAB + 8 * kq);
+                af[mt] = *reinterpret_cast<const bf16x8 *>(G + swz(16 * mt + col, 8 * kq));
             bf16x8 bfr[NT];
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
-                bfr[nt] = *reinterpret_cast<const bf16x8 *>(T + (size_t)(cbase + 16 * nt + col) * MX_NLAB +
-                                                                8 * kq);
+                bfr[nt] = *reinterpret_cast<const bf16x8 *>(T + swz(cbase + 16 * nt + col, 8 * kq));
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
