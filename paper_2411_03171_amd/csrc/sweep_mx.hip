@@ -291,7 +291,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     const float b1 = a.adam.b1, b2 = a.adam.b2, lr = a.adam.lr, eps = a.adam.eps;
     int pos = 0;              // first sorted key not below the current chunk
     uint32_t head = 0xffffffffu;   // tg[pos] (uniform), or the largest key past the end
-    if (tg_lds && nnz > 0) head = tg[0];
+    if (tg_lds && nnz > 0) head = __builtin_amdgcn_readfirstlane(tg[0]);
     int32_t c0 = 0, c1 = 0;   // T columns written by this lane in the previous chunk
 
     // One chunk: `cur` holds its rows and optimiser state, `nxt` receives the
@@ -323,7 +323,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             // the cursor only moves past keys of chunks already behind
             while ((head >> 6) < l0u) {
                 ++pos;
-                head = pos < nnz ? tg[pos] : 0xffffffffu;
+                head = pos < nnz ? __builtin_amdgcn_readfirstlane(tg[pos]) : 0xffffffffu;
             }
             if ((head >> 6) - l0u < (uint32_t)MX_NLAB) {
                 for (int e = pos; e < nnz; ++e) {
@@ -397,11 +397,14 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 const bool live = valid && 4 * u + e < a.B;
                 const float zz = z[e] + cur.b;
                 const float y = ((yw >> e) & 1u) ? 1.f : 0.f;
-                const float ex = __expf(-fabsf(zz));
+                // exp(-|z|) in (0, 1] and log(1 + exp(-|z|)) with the hardware
+                // base-2 exp and log (their arguments need no range reduction)
+                const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
                 const float opx = 1.f + ex;
                 const float r = __builtin_amdgcn_rcpf(opx);
                 const float sig = zz >= 0.f ? r : ex * r;
-                loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __logf(opx) : 0.f;
+                loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
+                                 : 0.f;
                 g[e] = live ? a.s * (sig - y) : 0.f;
             }
             // dW partials over the lane's rows, slot order r ^ Kp
