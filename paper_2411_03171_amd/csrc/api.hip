@@ -46,15 +46,21 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int max_parts_for(int num_cu) { return std::max(1, std::min(2 * num_cu, 1024)); }
 
-WsLayout ws_layout(int32_t d, int32_t B_max, int32_t nnz_max, int max_parts) {
+WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts) {
     WsLayout w{};
+    const int passes = (B_max + MX_PASS_B - 1) / MX_PASS_B;
     size_t off = 0;
     w.loss_part = off;
-    off = align256(off + sizeof(float) * (size_t)max_parts);
+    off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)passes);
     w.tgt_b = off;
     off = align256(off + sizeof(int32_t) * (size_t)std::max(nnz_max, 1));
     w.dx_part = off;
     off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)B_max * (size_t)d);
+    w.has_partial = B_max > MX_PASS_B && k == 32;
+    w.dwp = off;
+    if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L * (size_t)k);
+    w.dbp = off;
+    if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L);
     w.total = off;
     return w;
 }
@@ -144,7 +150,7 @@ size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max, int3
     if (check_shape(L, d, k, B_max, nnz_max)) return 0;
     int cu = 0, dev = 0;
     if (device_cu_count(&cu, &dev)) return 0;
-    return ws_layout(d, B_max, nnz_max, max_parts_for(cu)).total;
+    return ws_layout(L, d, k, B_max, nnz_max, max_parts_for(cu)).total;
 }
 
 int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype, void *W,
@@ -170,7 +176,7 @@ int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t
     rc = device_cu_count(&cu, &dev);
     if (rc) return rc;
     const int parts = max_parts_for(cu);
-    const WsLayout wl = ws_layout(d, B_max, nnz_max, parts);
+    const WsLayout wl = ws_layout(L, d, k, B_max, nnz_max, parts);
     if (workspace_bytes < wl.total)
         return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, wl.total);
     ffsl_layer *h = new (std::nothrow) ffsl_layer;

@@ -27,12 +27,17 @@ struct Layer {
 
 // Workspace carve-up (offsets in bytes, each 256-byte aligned).
 struct WsLayout {
-    size_t loss_part;   // float [max_parts]
+    size_t loss_part;   // float [max_parts * batch passes]
     size_t tgt_b;       // int32 [nnz_max]  sample of each positive pair
     size_t dx_part;     // float [max_parts][B_max][d]
+    size_t dwp, dbp;    // float [L][k], [L]: dW / dbias carried between the
+                        // batch passes of the fused fast path (B_max > 64, k = 32)
+    bool has_partial;
     size_t total;
 };
-WsLayout ws_layout(int32_t d, int32_t B_max, int32_t nnz_max, int max_parts);
+WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts);
+// samples per pass of the fused fast path
+constexpr int MX_PASS_B = 64;
 int max_parts_for(int num_cu);
 
 // ---------------------------------------------------------------- errors
@@ -98,7 +103,8 @@ struct SweepCall {
 
 int launch_sweep(const SweepCall &c);
 bool sweep_mx_eligible(const Layer &ly, int B, int mode);
-int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, int *grid_out);
+int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
+                    float *dbp, int *grid_out, int *passes_out);
 int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
                uint8_t *mask, int32_t *exhausted, hipStream_t st);

@@ -384,7 +384,8 @@ int launch_vt(int mode, const SweepArgs &a, size_t shm, int grid, hipStream_t st
 
 constexpr size_t LDS_BUDGET = 160 * 1024 - 4096;  // minus static arrays
 
-int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int grid, int B, int d);
+int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int nloss, int B, int d,
+                 int ndx);
 
 int launch_sweep(const SweepCall &c) {
     const Layer &ly = *c.layer;
@@ -398,7 +399,7 @@ int launch_sweep(const SweepCall &c) {
     if (T > SW_MAXT) return fail(FFSL_EUNSUPPORTED, "too many batch tiles (%d)", T);
     const size_t shm = (size_t)Bt * per_b + ym_bytes;
 
-    const WsLayout wl = ws_layout(d, ly.B_max, ly.nnz_max, ly.max_parts);
+    const WsLayout wl = ws_layout(ly.L, d, ly.k, ly.B_max, ly.nnz_max, ly.max_parts);
     SweepArgs a{};
     a.L = ly.L;
     a.d = d;
@@ -437,10 +438,13 @@ int launch_sweep(const SweepCall &c) {
     }
 
     // the fast path reads X in 16-byte rows
-    if (sweep_mx_eligible(ly, B, c.mode) && (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
-        int rc = launch_sweep_mx(c, a.tgt_b, a.loss_part, a.dx_part, &grid);
+    if (sweep_mx_eligible(ly, B, c.mode) && (B <= MX_PASS_B || wl.has_partial) &&
+        (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
+        int passes = 1;
+        int rc = launch_sweep_mx(c, a.tgt_b, a.loss_part, a.dx_part, reinterpret_cast<float *>(ly.ws + wl.dwp),
+                                 reinterpret_cast<float *>(ly.ws + wl.dbp), &grid, &passes);
         if (rc) return rc;
-        return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d);
+        return finish_sweep(c, a.loss_part, a.dx_part, grid * passes, B, d, grid);
     }
 
     if (ly.ev_start) {
@@ -454,14 +458,16 @@ int launch_sweep(const SweepCall &c) {
         hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d);
+    return finish_sweep(c, a.loss_part, a.dx_part, grid, B, d, grid);
 }
 
-// loss and dX from the per-workgroup partials of a sweep
-int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int grid, int B, int d) {
+// loss and dX from the per-workgroup partials of a sweep: nloss loss partials,
+// ndx dX partials of [B][d]
+int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int nloss, int B, int d,
+                 int ndx) {
     int rc;
     if (c.loss_out) {
-        hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, loss_part, grid, c.s, c.loss_out,
+        hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, loss_part, nloss, c.s, c.loss_out,
                            (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0);
         rc = check_launch("loss_reduce");
         if (rc) return rc;
@@ -472,11 +478,11 @@ int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_par
         if (n % 4 == 0 && (reinterpret_cast<uintptr_t>(c.dX_out) & 15u) == 0) {
             const int64_t n4 = n / 4;
             hipLaunchKernelGGL(k_dx_reduce4, dim3((unsigned)((n4 + 15) / 16)), dim3(256), 0, c.stream,
-                               reinterpret_cast<const float4 *>(dx_part), grid, n4,
+                               reinterpret_cast<const float4 *>(dx_part), ndx, n4,
                                reinterpret_cast<float4 *>(c.dX_out), accum);
         } else {
             const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
-            hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, grid, n, c.dX_out,
+            hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, ndx, n, c.dX_out,
                                accum);
         }
         rc = check_launch("dx_reduce");

@@ -1,7 +1,7 @@
-// Fused training step of the fixed fan-in layer for bf16 values, fan-in 32,
-// batches of up to 64 samples and input widths that are a multiple of 128 up to 768
-// (the gathered forward, BCE, dW, dbias, dX and Adam of Sec. 2.2, in one
-// pass over the [L,k] arrays).
+// Fused training step of the fixed fan-in layer for bf16 values, fan-in 32 and
+// input widths that are a multiple of 128 up to 768 (the gathered forward,
+// BCE, dW, dbias, dX and Adam of Sec. 2.2, in one pass over the [L,k] arrays
+// per 64 samples of the batch; see launch_sweep_mx for larger batches).
 //
 // Workgroup: 512 threads (8 waves, two per SIMD), one per CU, persistent over
 // chunks of 32 label rows.  Sixteen lanes serve one row; lane u of a row owns
@@ -77,6 +77,18 @@ struct MxArgs {
     // array sizes in bytes: the range of each buffer resource, and the offset
     // that the chunk loop uses for an access that must not happen
     uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
+    // passes in dwp [L][32], dbp [L]
+    int32_t b0, Btot;
+    float *dwp, *dbp;
+};
+
+// what a batch pass does with the dW it has summed over its samples
+enum MxMode {
+    MX_ONLY = 0,    // the whole batch: Adam
+    MX_FIRST = 1,   // first of several passes: store the partial dW
+    MX_LAST = 2,    // last pass: add the carried partial, then Adam
+    MX_MIDDLE = 3,  // add the carried partial and store it again
 };
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
@@ -106,7 +118,7 @@ __device__ __forceinline__ void stf2(Rsrc r, uint32_t off, float2 x) {
 }
 
 struct Rsrcs {
-    Rsrc X, W, I, m, v, b, bm, bv;
+    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp;
 };
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -167,8 +179,10 @@ struct Prefetch {
     float b;           // its bias
 };
 
-// the chunk's rows and optimiser state, loaded a chunk ahead of their use; a
-// chunk or row past the end reads zeros
+// the chunk's rows and optimiser state (the moments only for a pass that
+// applies Adam), loaded a chunk ahead of their use; a chunk or row past the
+// end reads zeros
+template <bool MOMENTS>
 __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_t chunk, int tid, int lab, int u,
                                          int slot, Prefetch &p) {
     const int64_t l0 = chunk * MX_NLAB;
@@ -181,15 +195,21 @@ __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_
     const int64_t l = l0 + lab;
     const bool ok = live && l < a.L;
     const uint32_t om = ok ? (uint32_t)(l * MX_K + slot) * 4u : a.nb_m;
-    p.m = ldf2(R.m, om);
-    p.v = ldf2(R.v, om);
+    if constexpr (MOMENTS) {
+        p.m = ldf2(R.m, om);
+        p.v = ldf2(R.v, om);
+    } else {
+        p.m = p.v = make_float2(0.f, 0.f);
+    }
     p.b = ldf(R.b, ok ? (uint32_t)l * 4u : a.nb_b);
 }
 
 // NT = column tiles of 16 per wave: d = 128 * NT (a compile-time width keeps
 // the dX accumulators in fixed registers)
-template <int NT>
+template <int NT, int MODE>
 __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
+    constexpr bool ADAM = MODE == MX_ONLY || MODE == MX_LAST;      // updates W, m, v, bias
+    constexpr bool CARRY_IN = MODE == MX_LAST || MODE == MX_MIDDLE;
     extern __shared__ __align__(16) unsigned char lds[];
     constexpr int d = 128 * NT;
     unsigned char *Xs = lds;                                                // d * 128
@@ -220,9 +240,11 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     R.b = make_rsrc(a.bias, a.nb_b);
     R.bm = make_rsrc(a.bm, a.nb_b);
     R.bv = make_rsrc(a.bv, a.nb_b);
+    R.dwp = make_rsrc(a.dwp, MODE == MX_ONLY ? 0u : a.nb_m);
+    R.dbp = make_rsrc(a.dbp, MODE == MX_ONLY ? 0u : a.nb_b);
 
     Prefetch pa, pb;
-    prefetch(a, R, blockIdx.x, tid, lab, u, Kown, pa);
+    prefetch<ADAM>(a, R, blockIdx.x, tid, lab, u, Kown, pa);
 
     // stage X transposed (b fastest) and zero past B; clear T
     {
@@ -232,7 +254,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         const int b = lane;
 #pragma unroll 6
         for (int gi = wave; gi < d / 8; gi += MX_THREADS / 64) {
-            const uint32_t ox = b < a.B ? (uint32_t)(b * d + 8 * gi) * 2u : a.nb_X;
+            const uint32_t ox = b < a.B ? (uint32_t)((a.b0 + b) * d + 8 * gi) * 2u : a.nb_X;
             const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.X, ox, 0, 0);
             const uint32_t w4[4] = {q[0], q[1], q[2], q[3]};
 #pragma unroll
@@ -254,8 +276,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             uint32_t key = 0xffffffffu;
             if (e < nnz) {
                 const int32_t lb = a.tgt_lab[e];
-                const int32_t sb = a.tgt_b[e];
-                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < MX_NB) key = ((uint32_t)lb << 6) | (uint32_t)sb;
+                const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
+                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B) key = ((uint32_t)lb << 6) | (uint32_t)sb;
             }
             tg[e] = key;
         }
@@ -307,7 +329,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             Ws[tid] = cur.wv;
             if (!tg_lds && tid < MX_NLAB * 2) ym[tid] = 0u;
         }
-        prefetch(a, R, chunk + gridDim.x, tid, lab, u, Kown, nxt);
+        prefetch<ADAM>(a, R, chunk + gridDim.x, tid, lab, u, Kown, nxt);
         __syncthreads();
         // Every wave has read the previous chunk's G and T fragments before the
         // barrier above, so this lane's T entries of that chunk can be cleared;
@@ -336,8 +358,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         } else {
             for (int e = tid; e < nnz; e += MX_THREADS) {
                 const uint32_t ll = (uint32_t)a.tgt_lab[e] - l0u;
-                const uint32_t b = (uint32_t)a.tgt_b[e];
-                if (ll < MX_NLAB && b < MX_NB) atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
+                const uint32_t b = (uint32_t)(a.tgt_b[e] - a.b0);
+                if (ll < MX_NLAB && b < (uint32_t)a.B) atomicOr(&ym[ll * 2 + (b >> 5)], 1u << (b & 31));
             }
             __syncthreads();
             yrow = (uint64_t)ym[lab * 2] | ((uint64_t)ym[lab * 2 + 1] << 32);
@@ -353,7 +375,19 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             const bool valid = l < a.L;
             // the bias moments, used on lane u = 0 at the end of the row's work
             const uint32_t obm = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
-            const float bmcur = ldf(R.bm, obm), bvcur = ldf(R.bv, obm);
+            float bmcur = 0.f, bvcur = 0.f;
+            if constexpr (ADAM) {
+                bmcur = ldf(R.bm, obm);
+                bvcur = ldf(R.bv, obm);
+            }
+            // dW and dbias of this row summed over the earlier batch passes
+            const uint32_t odw = valid ? (uint32_t)(l * MX_K + Kown) * 4u : a.nb_m;
+            float2 dprev = make_float2(0.f, 0.f);
+            float dbprev = 0.f;
+            if constexpr (CARRY_IN) {
+                dprev = ldf2(R.dwp, odw);
+                dbprev = ldf(R.dbp, obm);
+            }
 
             // row data in the lane's slot order: register r <-> slot r ^ K (a row
             // past L has zero offsets and weights)
@@ -423,9 +457,10 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             // keeps its two
 #pragma unroll
             for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[r]);
-            const float dw0 = odd ? pw[2] : pw[0], dw1 = odd ? pw[3] : pw[1];
+            const float dw0 = (odd ? pw[2] : pw[0]) + dprev.x, dw1 = (odd ? pw[3] : pw[1]) + dprev.y;
+            if constexpr (!ADAM) stf2(R.dwp, odw, make_float2(dw0, dw1));
             // Adam on slots Kown, Kown+1
-            {
+            if constexpr (ADAM) {
                 float m0 = cur.m.x, m1 = cur.m.y, v0 = cur.v.x, v1 = cur.v.y;
                 const float w0 = __uint_as_float(wpair_own << 16);
                 const float w1 = __uint_as_float(wpair_own & 0xffff0000u);
@@ -442,12 +477,16 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 sg = add_dpp<DPP_ROW_MIRROR>(sg, sg);
                 sg = add_dpp<DPP_ROW_HALF_MIRROR>(sg, sg);
                 sg = add_dpp<DPP_QUAD_3210>(sg, sg);
-                sg = add_dpp<DPP_QUAD_1032>(sg, sg);
-                float mm = bmcur, vv = bvcur;
-                const float nb = adam_step(cur.b, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
-                stf(R.b, obm, nb);
-                stf(R.bm, obm, mm);
-                stf(R.bv, obm, vv);
+                sg = add_dpp<DPP_QUAD_1032>(sg, sg) + dbprev;
+                if constexpr (ADAM) {
+                    float mm = bmcur, vv = bvcur;
+                    const float nb = adam_step(cur.b, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                    stf(R.b, obm, nb);
+                    stf(R.bm, obm, mm);
+                    stf(R.bv, obm, vv);
+                } else {
+                    stf(R.dbp, obm, sg);
+                }
             }
             // dX inputs: g and the old weights (a row past L writes zeros at column 0)
 #pragma unroll
@@ -489,7 +528,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
 
     // write this workgroup's dX partial [B][d]
     {
-        float *P = a.dx_part + (size_t)blockIdx.x * a.B * d;
+        float *P = a.dx_part + ((size_t)blockIdx.x * a.Btot + a.b0) * d;
         const int col = lane & 15, kq = lane >> 4;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
@@ -518,10 +557,20 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
 constexpr int MX_NT_MAX = 6;    // widest input: 768 columns
 
 typedef void (*MxKernel)(const MxArgs);
-const MxKernel *mx_kernels() {
-    static const MxKernel k[MX_NT_MAX] = {k_sweep_mx<1>, k_sweep_mx<2>, k_sweep_mx<3>,
-                                          k_sweep_mx<4>, k_sweep_mx<5>, k_sweep_mx<6>};
-    return k;
+template <int NT>
+struct MxModes {
+    static constexpr MxKernel k[4] = {k_sweep_mx<NT, MX_ONLY>, k_sweep_mx<NT, MX_FIRST>, k_sweep_mx<NT, MX_LAST>,
+                                      k_sweep_mx<NT, MX_MIDDLE>};
+};
+MxKernel mx_kernel(int nt, int mode) {
+    switch (nt) {
+    case 1: return MxModes<1>::k[mode];
+    case 2: return MxModes<2>::k[mode];
+    case 3: return MxModes<3>::k[mode];
+    case 4: return MxModes<4>::k[mode];
+    case 5: return MxModes<5>::k[mode];
+    default: return MxModes<6>::k[mode];
+    }
 }
 
 size_t sweep_mx_lds(int d) {
@@ -532,16 +581,21 @@ size_t sweep_mx_lds(int d) {
 }  // namespace
 
 bool sweep_mx_eligible(const Layer &ly, int B, int mode) {
-    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && ly.k == MX_K && B <= MX_NB && ly.d % 128 == 0 &&
+    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && ly.k == MX_K && B <= FFSL_MAX_B && ly.d % 128 == 0 &&
            ly.d >= 128 && ly.d <= 128 * MX_NT_MAX && ly.L < ((int64_t)1 << 25) && sweep_mx_lds(ly.d) <= 160 * 1024;
 }
 
-int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, int *grid_out) {
+// Batches of up to 64 samples take one pass.  A larger batch is split into
+// passes of 64 samples: every pass accumulates its samples' dX rows and loss,
+// the first stores its dW / dbias in the carry buffers, middle passes add to
+// them, and the last adds its share and applies Adam.  W, the moments and the
+// bias change only in the last pass, so every pass sees the step's old state.
+int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
+                    float *dbp, int *grid_out, int *passes_out) {
     const Layer &ly = *c.layer;
     MxArgs a{};
     a.L = ly.L;
     a.d = ly.d;
-    a.B = c.B;
     a.nnz = c.nnz;
     a.nchunks = (ly.L + MX_NLAB - 1) / MX_NLAB;
     a.X = static_cast<const uint16_t *>(c.X);
@@ -556,31 +610,41 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.tgt_lab = c.tgt_lab;
     a.s = c.s;
     a.adam = c.adam;
-    a.loss_part = loss_part;
     a.dx_part = dx_part;
+    a.dwp = dwp;
+    a.dbp = dbp;
+    a.Btot = c.B;
     a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * MX_K * 2);
     a.nb_I = (uint32_t)(ly.L * MX_K * 4);
     a.nb_m = (uint32_t)(ly.L * MX_K * 4);
     a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
     const size_t shm = sweep_mx_lds(ly.d);
-    const MxKernel kern = mx_kernels()[ly.d / 128 - 1];
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     const int grid = (int)std::min<int64_t>(a.nchunks, std::min(ly.max_parts, ly.num_cu));
+    const int passes = (c.B + MX_NB - 1) / MX_NB;
     if (ly.ev_start) {
-        e = hipEventRecord(ly.ev_start, c.stream);
+        hipError_t e = hipEventRecord(ly.ev_start, c.stream);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(MX_THREADS), shm, c.stream, a);
-    int rc = check_launch("sweep_mx");
-    if (rc) return rc;
+    for (int p = 0; p < passes; ++p) {
+        const int mode = passes == 1 ? MX_ONLY : p == 0 ? MX_FIRST : p == passes - 1 ? MX_LAST : MX_MIDDLE;
+        a.b0 = p * MX_NB;
+        a.B = std::min(MX_NB, c.B - a.b0);
+        a.loss_part = loss_part + (size_t)p * grid;
+        const MxKernel kern = mx_kernel(ly.d / 128, mode);
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(MX_THREADS), shm, c.stream, a);
+        int rc = check_launch("sweep_mx");
+        if (rc) return rc;
+    }
     if (ly.ev_stop) {
-        e = hipEventRecord(ly.ev_stop, c.stream);
+        hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
     *grid_out = grid;
+    *passes_out = passes;
     return FFSL_OK;
 }
 
