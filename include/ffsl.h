@@ -72,9 +72,10 @@ FFSL_API int ffsl_version(void);
 
 /* Bytes of device workspace a layer of this shape needs for batches of up to
  * B_max samples with up to nnz_max positive (sample, label) pairs per batch.
- * Besides per-workgroup partial sums of the loss and dX (O(B_max * d)), a
- * layer with k = 32 and B_max > 64 gets 4*(L*k + L) bytes in which the fused
- * step carries dW and dbias between its passes of 64 samples.
+ * Besides per-workgroup partial sums of the loss and dX (O(B_max * d)), the
+ * fused step carries dW and dbias between passes over the batch in 4*(L*k + L)
+ * bytes: for k = 32 and B_max > 64 (passes of 64 samples), and for k = 64,
+ * d a multiple of 128 up to 2048, L < 2^24 and B_max > 16 (passes of 16).
  * Returns 0 for invalid shapes. */
 FFSL_API size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max,
                             int32_t nnz_max);

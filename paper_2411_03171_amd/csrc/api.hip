@@ -48,7 +48,9 @@ int max_parts_for(int num_cu) { return std::max(1, std::min(2 * num_cu, 1024)); 
 
 WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts) {
     WsLayout w{};
-    const int passes = (B_max + MX_PASS_B - 1) / MX_PASS_B;
+    const bool wide = wide_shape(L, d, k);
+    const int pass_b = wide ? WD_PASS_B : MX_PASS_B;
+    const int passes = (B_max + pass_b - 1) / pass_b;
     size_t off = 0;
     w.loss_part = off;
     off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)passes);
@@ -56,7 +58,7 @@ WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_m
     off = align256(off + sizeof(int32_t) * (size_t)std::max(nnz_max, 1));
     w.dx_part = off;
     off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)B_max * (size_t)d);
-    w.has_partial = B_max > MX_PASS_B && k == 32;
+    w.has_partial = (k == 32 && B_max > MX_PASS_B) || (wide && B_max > WD_PASS_B);
     w.dwp = off;
     if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L * (size_t)k);
     w.dbp = off;

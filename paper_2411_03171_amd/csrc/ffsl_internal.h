@@ -37,7 +37,12 @@ struct WsLayout {
 };
 WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts);
 // samples per pass of the fused fast path
-constexpr int MX_PASS_B = 64;
+constexpr int MX_PASS_B = 64;   // samples per pass of the fan-in-32 fast path
+constexpr int WD_PASS_B = 16;   // samples per pass of the wide fan-in-64 fast path
+// layers whose shape the wide fan-in-64 fast path serves (bf16 values)
+inline bool wide_shape(int64_t L, int32_t d, int32_t k) {
+    return k == 64 && d % 128 == 0 && d >= 128 && d <= 2048 && L < ((int64_t)1 << 24);
+}
 int max_parts_for(int num_cu);
 
 // ---------------------------------------------------------------- errors
@@ -105,6 +110,9 @@ int launch_sweep(const SweepCall &c);
 bool sweep_mx_eligible(const Layer &ly, int B, int mode);
 int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
                     float *dbp, int *grid_out, int *passes_out);
+bool sweep_wide_eligible(const Layer &ly, int mode);
+int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
+                      float *dbp, int *grid_out, int *passes_out);
 int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
                uint8_t *mask, int32_t *exhausted, hipStream_t st);

@@ -437,7 +437,15 @@ int launch_sweep(const SweepCall &c) {
         if (rc) return rc;
     }
 
-    // the fast path reads X in 16-byte rows
+    // the fast paths read X in 16-byte rows
+    if (sweep_wide_eligible(ly, c.mode) && (B <= WD_PASS_B || wl.has_partial) &&
+        (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
+        int passes = 1;
+        int rc = launch_sweep_wide(c, a.tgt_b, a.loss_part, a.dx_part, reinterpret_cast<float *>(ly.ws + wl.dwp),
+                                   reinterpret_cast<float *>(ly.ws + wl.dbp), &grid, &passes);
+        if (rc) return rc;
+        return finish_sweep(c, a.loss_part, a.dx_part, grid * passes, B, d, grid);
+    }
     if (sweep_mx_eligible(ly, B, c.mode) && (B <= MX_PASS_B || wl.has_partial) &&
         (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
         int passes = 1;

@@ -44,7 +44,7 @@
 // data-dependent branches and the compiler can keep exact counts of
 // outstanding memory operations (a branch around a store makes it drain them
 // all).
-#include "ffsl_internal.h"
+#include "sweep_dev.h"
 
 namespace ffsl {
 
@@ -57,9 +57,7 @@ constexpr int MX_NB = 64;       // padded batch
 constexpr int MX_XS = 128;      // bytes per X column row in LDS
 constexpr int MX_TG_MAX = 1024; // positives kept in LDS
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+using namespace fdev;
 
 struct MxArgs {
     int64_t L;
@@ -83,72 +81,12 @@ struct MxArgs {
     float *dwp, *dbp;
 };
 
-// what a batch pass does with the dW it has summed over its samples
-enum MxMode {
-    MX_ONLY = 0,    // the whole batch: Adam
-    MX_FIRST = 1,   // first of several passes: store the partial dW
-    MX_LAST = 2,    // last pass: add the carried partial, then Adam
-    MX_MIDDLE = 3,  // add the carried partial and store it again
-};
-
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-
-// raw buffer resource over [p, p + nbytes): out-of-range loads read 0 and
-// out-of-range stores are dropped
-__device__ __forceinline__ Rsrc make_rsrc(const void *p, uint32_t nbytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)nbytes, 0x00020000);
-}
-
-__device__ __forceinline__ uint32_t ld32(Rsrc r, uint32_t off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
-}
-__device__ __forceinline__ float ldf(Rsrc r, uint32_t off) { return __uint_as_float(ld32(r, off)); }
-__device__ __forceinline__ float2 ldf2(Rsrc r, uint32_t off) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
-    return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
-}
-__device__ __forceinline__ void st32(Rsrc r, uint32_t off, uint32_t x) {
-    __builtin_amdgcn_raw_buffer_store_b32(x, r, off, 0, 0);
-}
-__device__ __forceinline__ void stf(Rsrc r, uint32_t off, float x) { st32(r, off, __float_as_uint(x)); }
-__device__ __forceinline__ void stf2(Rsrc r, uint32_t off, float2 x) {
-    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 v = {__float_as_uint(x.x), __float_as_uint(x.y)};
-    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
-}
+// pass roles (see launch_sweep_mx)
+constexpr int MX_ONLY = PASS_ONLY, MX_FIRST = PASS_FIRST, MX_LAST = PASS_LAST, MX_MIDDLE = PASS_MIDDLE;
 
 struct Rsrcs {
     Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp;
 };
-
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
-                                           false);
-}
-
-// a.b with no accumulator (the three-operand form takes an inline zero)
-__device__ __forceinline__ float dot2z(uint32_t a, uint32_t b) {
-    float r;
-    asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-    bf16x2 p = {(__bf16)lo, (__bf16)hi};
-    return __builtin_bit_cast(uint32_t, p);
-}
-
-// x + (value of register `y` in the DPP partner lane)
-template <int CTRL>
-__device__ __forceinline__ float add_dpp(float x, float y) {
-    const int t = __builtin_amdgcn_update_dpp(0, __float_as_int(y), CTRL, 0xf, 0xf, false);
-    return x + __int_as_float(t);
-}
-
-constexpr int DPP_ROW_MIRROR = 0x140;       // lane j <- 15 - j within 16
-constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane j <- 7 - j within 8
-constexpr int DPP_QUAD_3210 = 0x1B;         // lane j <- j ^ 3 within 4
-constexpr int DPP_QUAD_1032 = 0xB1;         // lane j <- j ^ 1 within 4
 
 // G and T rows hold 32 bf16 (64 bytes = four 16-byte chunks).  The matrix-
 // core fragments read one chunk from each of 16 consecutive rows; stored
@@ -156,20 +94,6 @@ constexpr int DPP_QUAD_1032 = 0xB1;         // lane j <- j ^ 1 within 4
 // therefore kept at chunk q ^ ((r >> 2) & 3); element e of row r sits at:
 __device__ __forceinline__ int swz(int r, int e) {
     return r * MX_NLAB + ((((e >> 3) ^ (r >> 2)) & 3) << 3) + (e & 7);
-}
-
-__device__ __forceinline__ int lane_key(int u) {
-    return ((u & 1) ? 2 : 0) ^ ((u & 2) ? 6 : 0) ^ ((u & 4) ? 12 : 0) ^ ((u & 8) ? 24 : 0);
-}
-
-// Adam with the bias corrections folded into reciprocals; fp32 throughout
-__device__ __forceinline__ float adam_step(float p, float g, float &mm, float &vv, float b1, float b2,
-                                           float inv_bc1, float inv_bc2, float lr, float eps, float decay) {
-    p *= decay;
-    mm = b1 * mm + (1.f - b1) * g;
-    vv = b2 * vv + (1.f - b2) * g * g;
-    const float den = __builtin_amdgcn_sqrtf(vv * inv_bc2) + eps;
-    return p - (lr * inv_bc1) * mm * __builtin_amdgcn_rcpf(den);
 }
 
 struct Prefetch {

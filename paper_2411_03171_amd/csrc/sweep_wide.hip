@@ -1,0 +1,529 @@
+// Fused training step of the fixed fan-in layer for bf16 values, fan-in 64 and
+// wide inputs (d a multiple of 128 up to 2048, the intermediate-layer width):
+// the gathered forward, BCE, dW, dbias, dX and Adam of Sec. 2.2.
+//
+// At d = 2048 neither X for 64 samples (256 KB) nor a 32-row weight tile for
+// the dX product (128 KB) fits next to the other in the 160 KB of LDS, and a
+// dX accumulator of 64 samples (512 KB) exceeds the register file.  The batch
+// therefore runs in passes of 16 samples (see launch_sweep_wide), each one
+// sweep over the [L,k] arrays:
+//
+// Workgroup: 512 threads (8 waves), one per CU, persistent over chunks of 16
+// label rows.  Thirty-two lanes serve one row: lane u handles sample
+// b = u & 15 of the pass and the half h = u >> 4 of the row's 64 slots.
+//
+//   LDS  Xs [d][16] bf16   the pass's samples transposed (column i is 32
+//                          contiguous bytes), zero-padded past the pass
+//        T  [d][16] bf16   the chunk's weights scattered densely by column
+//        G  [16][16] bf16  the chunk's dlogits (both with the 8-byte quarters
+//                          of a row rotated every 4 rows, see qswz)
+//        Is, Ws            the chunk's index rows (as byte offsets into Xs)
+//                          and weight rows; each wave stages its own two rows
+//        tg                the pass's positives as sorted (label, sample) keys
+//
+//   1. gather: for each of its 32 slots the lane reads the 2 bytes
+//      X[b, I[l,j]], two slots packed per register: the pairs line up with
+//      the row's weight pairs, so the forward is one v_dot2 per slot pair,
+//      and the halves' partial sums meet with one v_permlane16_swap;
+//   2. BCE loss and dlogit g of (row, sample);
+//   3. dW: one v_dot2 per slot (g rounded to bf16) and the 16-lane
+//      reduce-scatter over the pass's samples (register r holds slot
+//      r ^ Kp(b) of the half; the lane keeps two slots);
+//   4. Adam on those two slots, streaming W, m, v back to HBM;
+//   5. dX: g and the old weights go to G and T, and the matrix cores add
+//      G x T^T (16 x 16 by 16 x d) into a per-workgroup dX in registers (each
+//      wave owns the 16-column tiles w, w+8, ...), written out at the end.
+// All HBM accesses of the chunk loop are range-checked buffer operations: a
+// row past L reads zeros and its writes are dropped.
+#include <utility>
+
+#include "sweep_dev.h"
+
+namespace ffsl {
+
+namespace {
+
+using namespace fdev;
+
+constexpr int WD_THREADS = 512;
+constexpr int WD_NLAB = 16;      // label rows per chunk
+constexpr int WD_K = 64;         // fan-in of this path
+constexpr int WD_NB = 16;        // samples per pass
+constexpr int WD_XS = 32;        // bytes per X column row in LDS
+constexpr int WD_TG_MAX = 1024;  // positives kept in LDS
+constexpr int WD_NT_MAX = 16;    // widest input: 2048 columns
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+struct WdArgs {
+    int64_t L;
+    int32_t d, B, nnz;
+    int64_t nchunks;
+    const uint16_t *X;
+    uint16_t *W;
+    const int32_t *I;
+    float *bias, *m, *v, *bm, *bv;
+    const int32_t *tgt_b, *tgt_lab;
+    float s;
+    AdamParams adam;
+    float *loss_part;
+    float *dx_part;
+    // array sizes in bytes: the range of each buffer resource, and the offset
+    // that the chunk loop uses for an access that must not happen
+    uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
+    // passes in dwp [L][64], dbp [L]
+    int32_t b0, Btot;
+    float *dwp, *dbp;
+};
+
+struct Rsrcs {
+    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp;
+};
+
+// G and T rows hold 16 bf16 (32 bytes = four 8-byte quarters).  A matrix-core
+// fragment reads one quarter from each of 16 consecutive rows; stored plainly,
+// rows r, r+4, ... would share banks.  Quarter q of row r is kept at quarter
+// q ^ ((r >> 2) & 3); element e of row r sits at:
+__device__ __forceinline__ int qswz(int r, int e) {
+    return r * 16 + ((((e >> 2) ^ (r >> 2)) & 3) << 2) + (e & 3);
+}
+
+struct Prefetch {
+    uint2 iv;          // two index words of the chunk's I rows
+    uint32_t wv;       // one weight word of the chunk's W rows
+    float2 m, v;       // moments of the lane's two slots of its row
+    float b;           // its bias
+};
+
+// the chunk's rows and optimiser state (the moments only for a pass that
+// applies Adam), loaded a chunk ahead of their use; a chunk or row past the
+// end reads zeros.  Lane tid loads words of row tid / 32 only: a row its wave
+// serves.
+template <bool MOMENTS>
+__device__ __forceinline__ void prefetch(const WdArgs &a, const Rsrcs &R, int64_t chunk, int tid, int lab,
+                                         int slot, Prefetch &p) {
+    const int64_t l0 = chunk * WD_NLAB;
+    const bool live = chunk < a.nchunks;
+    const auto iv = __builtin_amdgcn_raw_buffer_load_b64(R.I, live ? (uint32_t)(l0 * WD_K * 4) + 8u * tid : a.nb_I,
+                                                         0, 0);
+    p.iv = make_uint2(iv[0], iv[1]);
+    p.wv = ld32(R.W, live ? (uint32_t)(l0 * WD_K * 2) + 4u * tid : a.nb_W);
+    const int64_t l = l0 + lab;
+    const bool ok = live && l < a.L;
+    const uint32_t om = ok ? (uint32_t)(l * WD_K + slot) * 4u : a.nb_m;
+    if constexpr (MOMENTS) {
+        p.m = ldf2(R.m, om);
+        p.v = ldf2(R.v, om);
+    } else {
+        p.m = p.v = make_float2(0.f, 0.f);
+    }
+    p.b = ldf(R.b, ok ? (uint32_t)l * 4u : a.nb_b);
+}
+
+// NT = d / 128: the d / 16 column tiles of 16 are dealt to the 8 waves, NT each
+template <int NT, int MODE>
+__global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
+    constexpr bool ADAM = MODE == PASS_ONLY || MODE == PASS_LAST;      // updates W, m, v, bias
+    constexpr bool CARRY_IN = MODE == PASS_LAST || MODE == PASS_MIDDLE;
+    constexpr int d = 128 * NT;
+    extern __shared__ __align__(16) unsigned char lds[];
+    unsigned char *Xs = lds;                                                  // d * 32
+    uint16_t *T = reinterpret_cast<uint16_t *>(lds + (size_t)d * WD_XS);      // d * 16
+    uint16_t *G = T + (size_t)d * WD_NLAB;                                    // 16 * 16
+    int32_t *Is = reinterpret_cast<int32_t *>(G + WD_NB * WD_NLAB);          // 16 * 64
+    uint16_t *Ws = reinterpret_cast<uint16_t *>(Is + WD_NLAB * WD_K);        // 16 * 64
+    uint32_t *tg = reinterpret_cast<uint32_t *>(Ws + WD_NLAB * WD_K);        // WD_TG_MAX
+
+    const int tid = threadIdx.x;
+    const int lab = tid >> 5, u = tid & 31;
+    const int h = u >> 4, bs = u & 15;          // slot half, sample of the pass
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    // register r of the lane holds slot r ^ Kp of its half; the reduce-scatter
+    // leaves it with slots Kown, Kown + 1 of the half
+    const int Kp = lane_key(bs) & ~2;
+    const int Kown = Kp + 2 * (bs & 1);
+    const int myslot = 32 * h + Kown;
+    const bool odd = (bs & 1) != 0;
+    const int nnz = a.nnz;
+    const bool tg_lds = nnz <= WD_TG_MAX;
+    uint32_t *ymw = tg + 2 * wave;   // scan path: this wave's two rows' masks
+
+    Rsrcs R;
+    R.X = make_rsrc(a.X, a.nb_X);
+    R.W = make_rsrc(a.W, a.nb_W);
+    R.I = make_rsrc(a.I, a.nb_I);
+    R.m = make_rsrc(a.m, a.nb_m);
+    R.v = make_rsrc(a.v, a.nb_m);
+    R.b = make_rsrc(a.bias, a.nb_b);
+    R.bm = make_rsrc(a.bm, a.nb_b);
+    R.bv = make_rsrc(a.bv, a.nb_b);
+    R.dwp = make_rsrc(a.dwp, MODE == PASS_ONLY ? 0u : a.nb_m);
+    R.dbp = make_rsrc(a.dbp, MODE == PASS_ONLY ? 0u : a.nb_b);
+
+    Prefetch pa, pb;
+    prefetch<ADAM>(a, R, blockIdx.x, tid, lab, myslot, pa);
+
+    // stage the pass's samples transposed (sample fastest) and zero past B;
+    // clear T and G
+    {
+        uint16_t *X16 = reinterpret_cast<uint16_t *>(Xs);
+        const int b = lane & 15;
+        for (int gi = 4 * wave + (lane >> 4); gi < d / 8; gi += 4 * (WD_THREADS / 64)) {
+            const uint32_t ox = b < a.B ? (uint32_t)((a.b0 + b) * d + 8 * gi) * 2u : a.nb_X;
+            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.X, ox, 0, 0);
+            const uint32_t w4[4] = {q[0], q[1], q[2], q[3]};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                X16[(8 * gi + 2 * j) * WD_NB + b] = (uint16_t)(w4[j] & 0xffffu);
+                X16[(8 * gi + 2 * j + 1) * WD_NB + b] = (uint16_t)(w4[j] >> 16);
+            }
+        }
+        uint32_t *TG = reinterpret_cast<uint32_t *>(T);
+        for (int e = tid; e < (d * WD_NLAB + WD_NB * WD_NLAB) / 2; e += WD_THREADS) TG[e] = 0u;
+    }
+    // The pass's positives as keys (label << 4 | sample), sorted ascending
+    // (bitonic sort in LDS; a label outside [0,L) becomes the largest key and
+    // is never matched).  Chunks of one workgroup come in ascending order, so
+    // a cursor that only moves forward finds each chunk's positives.
+    if (tg_lds) {
+        int n2 = 1;
+        while (n2 < nnz) n2 <<= 1;
+        for (int e = tid; e < n2; e += WD_THREADS) {
+            uint32_t key = 0xffffffffu;
+            if (e < nnz) {
+                const int32_t lb = a.tgt_lab[e];
+                const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
+                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B) key = ((uint32_t)lb << 4) | (uint32_t)sb;
+            }
+            tg[e] = key;
+        }
+        __syncthreads();
+        for (int k = 2; k <= n2; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int i = tid; i < n2; i += WD_THREADS) {
+                    const int ij = i ^ j;
+                    if (ij > i) {
+                        const uint32_t x = tg[i], y = tg[ij];
+                        if (((i & k) == 0) ? (x > y) : (x < y)) {
+                            tg[i] = y;
+                            tg[ij] = x;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+    __syncthreads();
+
+    // dX accumulators: the 16 samples x NT column tiles of 16 of this wave
+    f32x4 acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    float loss_acc = 0.f;
+    const float decay = 1.f - a.adam.lr * a.adam.wd;
+    const float inv_bc1 = 1.f / a.adam.bc1, inv_bc2 = 1.f / a.adam.bc2;
+    const float b1 = a.adam.b1, b2 = a.adam.b2, lr = a.adam.lr, eps = a.adam.eps;
+    int pos = 0;              // first sorted key not below the current chunk
+    uint32_t head = 0xffffffffu;   // tg[pos] (uniform), or the largest key past the end
+    if (tg_lds && nnz > 0) head = __builtin_amdgcn_readfirstlane(tg[0]);
+    int32_t c0 = 0, c1 = 0;   // T columns written by this lane in the previous chunk
+    const int kk = lab;       // the row within the chunk
+
+    // One chunk: `cur` holds its rows and optimiser state, `nxt` receives the
+    // next chunk's.
+    auto step = [&](int64_t chunk, const Prefetch &cur, Prefetch &nxt) {
+        const int64_t l0 = chunk * WD_NLAB;
+        const uint32_t l0u = (uint32_t)l0;   // L < 2^24: label offsets fit in 32 bits
+
+        // stage this wave's rows: indices become clamped byte offsets of X columns
+        {
+            const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
+            *reinterpret_cast<int2 *>(Is + 2 * tid) = make_int2(i0 * WD_XS, i1 * WD_XS);
+            reinterpret_cast<uint32_t *>(Ws)[tid] = cur.wv;
+        }
+        prefetch<ADAM>(a, R, chunk + gridDim.x, tid, lab, myslot, nxt);
+
+        // targets of this lane's row as a 16-bit sample mask
+        uint32_t yrow = 0;
+        if (tg_lds) {
+            while ((head >> 4) < l0u) {
+                ++pos;
+                head = pos < nnz ? __builtin_amdgcn_readfirstlane(tg[pos]) : 0xffffffffu;
+            }
+            if ((head >> 4) - l0u < (uint32_t)WD_NLAB) {
+                for (int e = pos; e < nnz; ++e) {
+                    const uint32_t key = tg[e];
+                    const uint32_t ll = (key >> 4) - l0u;
+                    if (ll >= (uint32_t)WD_NLAB) break;
+                    if (ll == (uint32_t)lab) yrow |= 1u << (key & 15u);
+                }
+            }
+            wave_lds_sync();
+        } else {
+            // each wave scans the whole target list for its two rows
+            if (lane < 2) ymw[lane] = 0u;
+            wave_lds_sync();
+            const uint32_t r0 = l0u + 2u * (uint32_t)wave;
+            for (int e = lane; e < nnz; e += 64) {
+                const uint32_t ll = (uint32_t)a.tgt_lab[e] - r0;
+                const uint32_t b = (uint32_t)(a.tgt_b[e] - a.b0);
+                if (ll < 2u && b < (uint32_t)a.B) atomicOr(&ymw[ll], 1u << b);
+            }
+            wave_lds_sync();
+            yrow = ymw[lab & 1];
+        }
+        int rl = lab;            // the row of the chunk this lane serves
+        int k4 = Kp >> 2;        // quad order of this lane
+        // opaque per chunk, so the per-slot LDS addresses are formed where
+        // they are used instead of being held in registers across chunks
+        asm volatile("" : "+v"(rl), "+v"(k4));
+        const int64_t l = l0 + rl;
+        const bool valid = l < a.L;
+        const uint32_t obm = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
+        float bmcur = 0.f, bvcur = 0.f;
+        if constexpr (ADAM) {
+            bmcur = ldf(R.bm, obm);
+            bvcur = ldf(R.bv, obm);
+        }
+        const uint32_t odw = valid ? (uint32_t)(l * WD_K + myslot) * 4u : a.nb_m;
+        float2 dprev = make_float2(0.f, 0.f);
+        float dbprev = 0.f;
+        if constexpr (CARRY_IN) {
+            dprev = ldf2(R.dwp, odw);
+            dbprev = ldf(R.dbp, obm);
+        }
+
+        // gather the lane's 32 slots as bf16 pairs (register p <-> slots
+        // 2p ^ Kp, (2p ^ Kp) + 1 of the half) and run the forward on the fly
+        uint32_t xp[16];
+        int32_t c0n = 0, c1n = 0;
+        uint32_t wown = 0u;
+        float za = 0.f, zb = 0.f;
+        const int32_t *Ish = Is + rl * WD_K + 32 * h;
+        const uint32_t *Wsh = reinterpret_cast<const uint32_t *>(Ws) + rl * (WD_K / 2) + 16 * h;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int qq = q ^ k4;   // pairs 2q, 2q+1 hold slots 4qq..4qq+3 of the half
+            const int4 iv = *reinterpret_cast<const int4 *>(Ish + 4 * qq);
+            const uint2 wv = *reinterpret_cast<const uint2 *>(Wsh + 2 * qq);
+            if (q == 0) {   // the lane's own slots are the first pair (odd: the second)
+                c0n = (odd ? iv.z : iv.x) / WD_XS;
+                c1n = (odd ? iv.w : iv.y) / WD_XS;
+                wown = odd ? wv.y : wv.x;
+            }
+            bf16x2 p0, p1;
+            p0[0] = *reinterpret_cast<const __bf16 *>(Xs + iv.x + 2 * bs);
+            p0[1] = *reinterpret_cast<const __bf16 *>(Xs + iv.y + 2 * bs);
+            p1[0] = *reinterpret_cast<const __bf16 *>(Xs + iv.z + 2 * bs);
+            p1[1] = *reinterpret_cast<const __bf16 *>(Xs + iv.w + 2 * bs);
+            xp[2 * q] = __builtin_bit_cast(uint32_t, p0);
+            xp[2 * q + 1] = __builtin_bit_cast(uint32_t, p1);
+            za = dot2(xp[2 * q], wv.x, za);
+            zb = dot2(xp[2 * q + 1], wv.y, zb);
+        }
+        // the two halves of the row add up their partial sums
+        const float zz = cross_rows_add(za + zb, za + zb) + cur.b;
+        // BCE and dlogit of (row, sample); zero for padded samples and rows
+        // past L; the loss is counted once, in half 0
+        const bool live = valid && bs < a.B;
+        const float y = ((yrow >> bs) & 1u) ? 1.f : 0.f;
+        const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
+        const float opx = 1.f + ex;
+        const float rr = __builtin_amdgcn_rcpf(opx);
+        const float sig = zz >= 0.f ? rr : ex * rr;
+        loss_acc += live && h == 0 ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
+                                   : 0.f;
+        const float g = live ? a.s * (sig - y) : 0.f;
+        // dW partials of the lane's slots, slot order r ^ Kp
+        const uint32_t glo = pack_bf16(g, 0.f), ghi = pack_bf16(0.f, g);
+        float pw[32];
+#pragma unroll
+        for (int p = 0; p < 16; ++p) {
+            pw[2 * p] = dot2z(xp[p], glo);
+            pw[2 * p + 1] = dot2z(xp[p], ghi);
+        }
+        // reduce-scatter over the pass's 16 samples
+        const float2 dws = reduce_scatter16(pw, odd);
+        const float dw0 = dws.x + dprev.x, dw1 = dws.y + dprev.y;
+        if constexpr (!ADAM) stf2(R.dwp, odw, make_float2(dw0, dw1));
+        if constexpr (ADAM) {
+            float m0 = cur.m.x, m1 = cur.m.y, v0 = cur.v.x, v1 = cur.v.y;
+            const float w0 = __uint_as_float(wown << 16);
+            const float w1 = __uint_as_float(wown & 0xffff0000u);
+            const float n0 = adam_step(w0, dw0, m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+            const float n1 = adam_step(w1, dw1, m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+            const uint32_t o = (uint32_t)(l * WD_K + myslot);
+            stf2(R.m, valid ? 4u * o : a.nb_m, make_float2(m0, m1));
+            stf2(R.v, valid ? 4u * o : a.nb_m, make_float2(v0, v1));
+            st32(R.W, valid ? 2u * o : a.nb_W, pack_bf16(n0, n1));
+        }
+        // bias: sum of g over the pass's samples (half 0's lanes), lane u == 0
+        // updates
+        {
+            const float sg = sum16(g) + dbprev;
+            if constexpr (ADAM) {
+                float mm = bmcur, vv = bvcur;
+                const float nb = adam_step(cur.b, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
+                stf(R.b, obm, nb);
+                stf(R.bm, obm, mm);
+                stf(R.bv, obm, vv);
+            } else {
+                stf(R.dbp, obm, sg);
+            }
+        }
+        // Every wave has read the previous chunk's G and T fragments before
+        // this barrier, so this lane's T entries of that chunk can be cleared;
+        // the entries of one row are only ever touched by the wave that owns
+        // the row, in program order.
+        __syncthreads();
+        T[qswz(c0, kk)] = 0;
+        T[qswz(c1, kk)] = 0;
+        // dX inputs: g and the old weights (a row past L writes zeros at column 0)
+        if (h == 0) G[qswz(bs, kk)] = (uint16_t)(glo & 0xffffu);
+        T[qswz(c0n, kk)] = (uint16_t)(wown & 0xffffu);
+        T[qswz(c1n, kk)] = (uint16_t)(wown >> 16);
+        c0 = c0n;
+        c1 = c1n;
+        __syncthreads();
+        // dX += G (16 x 16) * T^T (16 x d) on the matrix cores for this wave's
+        // column tiles; the next chunk's barrier orders these fragment reads
+        // before any rewrite of G or T
+        {
+            const int col = lane & 15, kq = lane >> 4;
+            const s16x4 af = *reinterpret_cast<const s16x4 *>(G + qswz(col, 4 * kq));
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const s16x4 bfr = *reinterpret_cast<const s16x4 *>(T + qswz(16 * (wave + 8 * t) + col, 4 * kq));
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(af, bfr, acc[t], 0, 0, 0);
+            }
+        }
+    };
+
+    // two chunks per iteration, so the prefetch buffers swap roles instead of
+    // being copied (a copy would wait for the loads in flight)
+    for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += 2 * (int64_t)gridDim.x) {
+        step(chunk, pa, pb);
+        if (chunk + gridDim.x >= a.nchunks) break;
+        step(chunk + gridDim.x, pb, pa);
+    }
+
+    // write this workgroup's dX partial [B][d] (its rows of the pass)
+    {
+        float *P = a.dx_part + ((size_t)blockIdx.x * a.Btot + a.b0) * d;
+        const int col = lane & 15, kq = lane >> 4;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int i = 16 * (wave + 8 * t) + col;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int b = 4 * kq + r;
+                if (b < a.B) P[(size_t)b * d + i] = acc[t][r];
+            }
+        }
+    }
+    // loss: workgroup tree reduction in the (now unused) T tile
+    float *red = reinterpret_cast<float *>(T);
+    __syncthreads();
+    red[tid] = loss_acc;
+    __syncthreads();
+    for (int st = WD_THREADS / 2; st > 0; st >>= 1) {
+        if (tid < st) red[tid] += red[tid + st];
+        __syncthreads();
+    }
+    if (tid == 0) a.loss_part[blockIdx.x] = red[0];
+}
+
+typedef void (*WdKernel)(const WdArgs);
+template <int NT>
+struct WdModes {
+    static constexpr WdKernel k[4] = {k_sweep_wide<NT, PASS_ONLY>, k_sweep_wide<NT, PASS_FIRST>,
+                                      k_sweep_wide<NT, PASS_LAST>, k_sweep_wide<NT, PASS_MIDDLE>};
+};
+template <int... NTs>
+WdKernel wd_pick(int nt, int mode, std::integer_sequence<int, NTs...>) {
+    WdKernel r = nullptr;
+    ((nt == NTs + 1 ? (r = WdModes<NTs + 1>::k[mode], 0) : 0), ...);
+    return r;
+}
+WdKernel wd_kernel(int nt, int mode) { return wd_pick(nt, mode, std::make_integer_sequence<int, WD_NT_MAX>{}); }
+
+size_t sweep_wide_lds(int d) {
+    return (size_t)d * WD_XS + (size_t)d * WD_NLAB * 2 + WD_NB * WD_NLAB * 2 + WD_NLAB * WD_K * 4 +
+           WD_NLAB * WD_K * 2 + WD_TG_MAX * 4;
+}
+
+}  // namespace
+
+bool sweep_wide_eligible(const Layer &ly, int mode) {
+    static_assert(WD_NB == WD_PASS_B, "pass width");
+    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && wide_shape(ly.L, ly.d, ly.k) && ly.k == WD_K &&
+           ly.d <= 128 * WD_NT_MAX && sweep_wide_lds(ly.d) <= 160 * 1024;
+}
+
+// The batch runs in passes of 16 samples: every pass accumulates its samples'
+// dX rows and loss, the first stores its dW / dbias in the carry buffers,
+// middle passes add to them, and the last adds its share and applies Adam.
+// W, the moments and the bias change only in the last pass, so every pass
+// sees the step's old state.
+int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
+                      float *dbp, int *grid_out, int *passes_out) {
+    const Layer &ly = *c.layer;
+    WdArgs a{};
+    a.L = ly.L;
+    a.d = ly.d;
+    a.nnz = c.nnz;
+    a.nchunks = (ly.L + WD_NLAB - 1) / WD_NLAB;
+    a.X = static_cast<const uint16_t *>(c.X);
+    a.W = static_cast<uint16_t *>(ly.W);
+    a.I = ly.I;
+    a.bias = ly.bias;
+    a.m = ly.m;
+    a.v = ly.v;
+    a.bm = ly.bm;
+    a.bv = ly.bv;
+    a.tgt_b = tgt_b;
+    a.tgt_lab = c.tgt_lab;
+    a.s = c.s;
+    a.adam = c.adam;
+    a.dx_part = dx_part;
+    a.dwp = dwp;
+    a.dbp = dbp;
+    a.Btot = c.B;
+    a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
+    a.nb_W = (uint32_t)(ly.L * WD_K * 2);
+    a.nb_I = (uint32_t)(ly.L * WD_K * 4);
+    a.nb_m = (uint32_t)(ly.L * WD_K * 4);
+    a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
+    const size_t shm = sweep_wide_lds(ly.d);
+    const int grid = (int)std::min<int64_t>(a.nchunks, std::min(ly.max_parts, ly.num_cu));
+    const int passes = (c.B + WD_NB - 1) / WD_NB;
+    if (ly.ev_start) {
+        hipError_t e = hipEventRecord(ly.ev_start, c.stream);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    for (int p = 0; p < passes; ++p) {
+        const int mode = passes == 1 ? PASS_ONLY : p == 0 ? PASS_FIRST : p == passes - 1 ? PASS_LAST : PASS_MIDDLE;
+        a.b0 = p * WD_NB;
+        a.B = std::min(WD_NB, c.B - a.b0);
+        a.loss_part = loss_part + (size_t)p * grid;
+        const WdKernel kern = wd_kernel(ly.d / 128, mode);
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(WD_THREADS), shm, c.stream, a);
+        int rc = check_launch("sweep_wide");
+        if (rc) return rc;
+    }
+    if (ly.ev_stop) {
+        hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
+        if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    *grid_out = grid;
+    *passes_out = passes;
+    return FFSL_OK;
+}
+
+}  // namespace ffsl

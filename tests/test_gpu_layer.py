@@ -35,6 +35,14 @@ CASES = {
     # more positives per batch (about 1900) than the fast path keeps on chip
     "mxdense": synth.dataclasses.replace(synth.scaled(W1["c4_bf16_L3M"], L=700, name="mxdense"),
                                          mean_pos=30.0),
+    # the fused bf16 fan-in-64 wide path (passes of 16 samples): another width
+    # with a ragged last pass and a ragged chunk, a single pass at the
+    # narrowest width, and more positives per pass (about 1300) than it keeps
+    # on chip
+    "w1024": synth.scaled(W1["c3_inter2048_L1M"], L=777, d=1024, B=37, name="w1024"),
+    "w128": synth.scaled(W1["c3_inter2048_L1M"], L=301, d=128, B=16, name="w128"),
+    "wdense": synth.dataclasses.replace(synth.scaled(W1["c3_inter2048_L1M"], L=900, name="wdense"),
+                                        mean_pos=80.0),
 }
 
 
@@ -134,7 +142,8 @@ def fused_update_bound(r, inp, w, mn, vn, t, lr, b1=0.9, b2=0.999, eps=1e-8):
     return lr * (d_m + d_v)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2s", "c4s", "c5s", "mx200", "k5", "k100", "b1"])
+@pytest.mark.parametrize("name", ["c1", "c2s", "c3s", "c4s", "c5s", "mx200", "w1024", "w128", "wdense", "k5",
+                                  "k100", "b1"])
 @pytest.mark.parametrize("wd", [0.0, 1e-4])
 def test_unfused_step_and_fused_step(torch_cuda, name, wd):
     torch = torch_cuda
