@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
 
 def sweep_source_hash():
     h = hashlib.sha256()
-    for name in ("sweep.hip", "sweep_mx.hip", "ffsl_internal.h"):
+    for name in ("sweep.hip", "sweep_mx.hip", "sweep_dev.h", "ffsl_internal.h"):
         with open(os.path.join(ROOT, "paper_2411_03171_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -228,6 +228,15 @@ def cpu_baseline(w, inp, target_s=12.0):
     }
 
 
+def sweep_kernel_name(w):
+    """The kernel the library picks for the fused step of this workload."""
+    if w.value == "bf16" and w.k == 32 and w.d % 128 == 0 and 128 <= w.d <= 768:
+        return "k_sweep_mx (fused bf16 fan-in-32 path, %d pass(es) of 64 samples)" % ((w.B + 63) // 64)
+    if w.value == "bf16" and w.k == 64 and w.d % 128 == 0 and 128 <= w.d <= 2048 and w.L < (1 << 24):
+        return "k_sweep_wide (fused bf16 fan-in-64 path, %d pass(es) of 16 samples)" % ((w.B + 15) // 16)
+    return "k_sweep (fused mode)"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -238,6 +247,9 @@ def main():
     ap.add_argument("--set-reps", type=int, default=10)
     ap.add_argument("--dense-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sparse-only", action="store_true",
+                    help="for a workload with dense parts, time its sparse layer alone (at the "
+                         "layer's own input width)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
@@ -260,9 +272,11 @@ def main():
     dev = "cuda:0"
     w = synth.WORKLOADS[args.workload]
     if w.din or w.aux_clusters:
-        print("bench.py: workload %s has dense parts; the fused-step bench runs the sparse "
-              "workloads" % w.name, file=sys.stderr)
-        sys.exit(2)
+        if not args.sparse_only:
+            print("bench.py: workload %s has dense parts; the fused-step bench runs the sparse "
+                  "workloads (or the sparse layer alone with --sparse-only)" % w.name, file=sys.stderr)
+            sys.exit(2)
+        w = synth.dataclasses.replace(w, din=0, aux_clusters=0)
     print("[bench] generating %s (L=%d k=%d B=%d d=%d %s)" % (w.name, w.L, w.k, w.B, w.d, w.value),
           file=sys.stderr, flush=True)
     inp = synth.make_layer_inputs(w, args.seed)
@@ -377,7 +391,7 @@ def main():
                    "positives_mean": w.mean_pos, "zipf_s": w.zipf_s},
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_sweep_mx (fused bf16 fan-in-32 path)" if (w.value == "bf16" and w.k == 32 and w.B <= 64) else "k_sweep (fused mode)",
+            "kernel": sweep_kernel_name(w),
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
