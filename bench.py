@@ -361,6 +361,29 @@ def main():
     print("[bench] SET: %.3f ms median, %.0f GB/s algorithmic, exhausted rows %d" %
           (set_ms_med, set_gbs, int(exhausted.cpu()[0])), file=sys.stderr, flush=True)
 
+    # SET fused into a training step (one call) against a plain step, both
+    # timed alone with events: the marginal cost of a SET step
+    def one_step(fn):
+        a, b = ev.create(), ev.create()
+        ev.record(a, stream)
+        fn()
+        ev.record(b, stream)
+        torch.cuda.synchronize()
+        return ev.elapsed_ms(a, b)
+
+    plain_ms, fused_ms = [], []
+    for r in range(args.set_reps):
+        t += 1
+        plain_ms.append(one_step(lambda: layer.train_step(X, off, lab, t=t, loss_out=loss, dX_out=dX)))
+        t += 1
+        fused_ms.append(one_step(lambda: layer.train_step_set(X, off, lab, t=t, frac=w.set_frac, seed=args.seed,
+                                                              set_round=1000 + r, loss_out=loss, dX_out=dX,
+                                                              mask=False, exhausted_out=exhausted)))
+    plain_med = sorted(plain_ms)[len(plain_ms) // 2]
+    fused_med = sorted(fused_ms)[len(fused_ms) // 2]
+    print("[bench] step with SET in one call: %.3f ms median (plain step %.3f ms): SET adds %.3f ms" %
+          (fused_med, plain_med, fused_med - plain_med), file=sys.stderr, flush=True)
+
     dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
@@ -409,6 +432,12 @@ def main():
             "unit": "GB/s",
             "frac": set_gbs / HBM_PEAK_GBS,
             "prune_per_row": n_set,
+        },
+        "set_in_step": {
+            "ms_median": fused_med,
+            "plain_step_ms_median": plain_med,
+            "marginal_ms": fused_med - plain_med,
+            "note": "ffsl_train_step_set: SET applied in the sweep that applies Adam",
         },
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],

@@ -159,6 +159,22 @@ FFSL_API int ffsl_train_step(ffsl_layer *layer, const void *X, int32_t B,
                     float eps, float wd, float *loss_out, float *dX_out,
                     uint32_t flags, void *stream);
 
+/* One fused training step followed by SET prune-and-regrow: the same result
+ * as ffsl_train_step(...) and then ffsl_set_update(layer, frac, seed,
+ * set_round, pruned_mask_out, exhausted_out) on the same stream (Sec. 2.1:
+ * the prune-regrow cycle runs between training steps).  On the fused bf16
+ * fan-in-32 path with at most 8 pruned slots per row the sweep that applies
+ * Adam also selects, regrows and zero-initialises, and rewrites each row's
+ * index words once; elsewhere the two calls run back to back.  The keys are
+ * those of the updated, stored weights.  Errors are those of both calls,
+ * reported before anything is launched. */
+FFSL_API int ffsl_train_step_set(ffsl_layer *layer, const void *X, int32_t B,
+                    const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz,
+                    float s, int64_t t, float lr, float beta1, float beta2,
+                    float eps, float wd, float *loss_out, float *dX_out,
+                    uint32_t flags, float frac, uint64_t seed, uint64_t set_round,
+                    uint8_t *pruned_mask_out, int32_t *exhausted_out, void *stream);
+
 /* SET prune-and-regrow (Sec. 2.1: magnitude pruning, random regrowth of as
  * many inactive weights; Appendix "Hyperparameter Settings": random growth
  * with zero initialisation), row by row so the fan-in stays exactly k:

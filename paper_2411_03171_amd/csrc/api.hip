@@ -300,6 +300,49 @@ int ffsl_train_step(ffsl_layer *layer, const void *X, int32_t B, const int32_t *
     return launch_sweep(c);
 }
 
+int ffsl_train_step_set(ffsl_layer *layer, const void *X, int32_t B, const int32_t *tgt_off,
+                        const int32_t *tgt_lab, int32_t nnz, float s, int64_t t, float lr, float beta1, float beta2,
+                        float eps, float wd, float *loss_out, float *dX_out, uint32_t flags, float frac,
+                        uint64_t seed, uint64_t set_round, uint8_t *pruned_mask_out, int32_t *exhausted_out,
+                        void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    const Layer &ly = layer->ly;
+    int rc = check_batch(ly, X, B, tgt_off, tgt_lab, nnz);
+    if (rc) return rc;
+    if (!(frac >= 0.f && frac <= 1.f)) return fail(FFSL_EINVAL, "frac must be in [0,1] (got %g)", (double)frac);
+    const int32_t n = (int32_t)floor((double)frac * (double)ly.k + 1e-9);
+    if (n > ly.d - ly.k)
+        return fail(FFSL_EINVAL, "cannot regrow %d weights per row: only %d inactive columns", n, ly.d - ly.k);
+    SweepCall c{};
+    rc = check_adam(t, lr, beta1, beta2, eps, wd, &c.adam);
+    if (rc) return rc;
+    c.layer = &ly;
+    c.X = X;
+    c.B = B;
+    c.tgt_off = tgt_off;
+    c.tgt_lab = tgt_lab;
+    c.nnz = nnz;
+    c.s = s;
+    c.mode = SWEEP_FUSED;
+    c.loss_out = loss_out;
+    c.dX_out = dX_out;
+    c.flags = flags;
+    c.stream = static_cast<hipStream_t>(stream);
+    c.set_n = n;
+    c.set_seed = seed;
+    c.set_round = set_round;
+    c.set_mask = pruned_mask_out;
+    c.set_exhausted = exhausted_out;
+    bool fused = false;
+    c.set_fused = &fused;
+    rc = launch_sweep(c);
+    if (rc || fused) return rc;
+    // the step's path has no fused SET: the same update as a separate call
+    if (n == 0 && !pruned_mask_out) return FFSL_OK;
+    return launch_set(ly, n, seed, set_round, pruned_mask_out, exhausted_out, static_cast<hipStream_t>(stream));
+}
+
 int ffsl_set_update(ffsl_layer *layer, float frac, uint64_t seed, uint64_t set_round, uint8_t *pruned_mask_out,
                     int32_t *exhausted_out, void *stream) {
     g_err.clear();

@@ -104,6 +104,13 @@ struct SweepCall {
     float *dX_out;
     uint32_t flags;
     hipStream_t stream;
+    // SET after the update (ffsl_train_step_set): n pruned per row (0: none);
+    // *set_fused is set when the sweep applied it
+    int32_t set_n;
+    uint64_t set_seed, set_round;
+    uint8_t *set_mask;
+    int32_t *set_exhausted;
+    bool *set_fused;
 };
 
 int launch_sweep(const SweepCall &c);

@@ -19,36 +19,15 @@
 //     order, with W = +0 and m = v = 0; all other slots are left untouched.
 #include <type_traits>
 
-#include "ffsl_internal.h"
+#include "sweep_dev.h"
 
 namespace ffsl {
 
 namespace {
 
-constexpr uint64_t SET_KEY_HI = 0x5345545F52454752ull;  // "SET_REGR"
 constexpr int SET_MAX_ROWS = 256;
-
-// Philox4x64-10 round structure: two 64x64->128 multiplies per round, the
-// high halves mixed with the other counter words and the round key, the key
-// advanced by the Weyl increments (golden ratio, sqrt(3)-1) between rounds.
-__device__ __forceinline__ void philox4x64_10(uint64_t &c0, uint64_t &c1, uint64_t &c2,
-                                              uint64_t &c3, uint64_t k0, uint64_t k1) {
-    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
-    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-#pragma unroll
-    for (int r = 0; r < 10; ++r) {
-        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
-        const uint64_t n0 = hi1 ^ c1 ^ k0;
-        const uint64_t n2 = hi0 ^ c3 ^ k1;
-        c0 = n0;
-        c1 = lo1;
-        c2 = n2;
-        c3 = lo0;
-        k0 += W0;
-        k1 += W1;
-    }
-}
+using fdev::philox4x64_10;
+using fdev::SET_KEY_HI;
 
 struct SetArgs {
     int64_t L;

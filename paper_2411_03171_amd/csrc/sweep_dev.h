@@ -1,6 +1,7 @@
-// Device helpers shared by the fused fast sweeps (sweep_mx.hip, sweep_wide.hip):
-// range-checked raw buffer access, bf16 dot products, DPP-fused adds, the
-// slot key of the 16-lane dW reduce-scatter and the Adam update.
+// Device helpers shared by the fused fast sweeps (sweep_mx.hip, sweep_wide.hip)
+// and SET (set.hip): range-checked raw buffer access, bf16 dot products,
+// DPP-fused adds, the slot key of the 16-lane dW reduce-scatter, the Adam
+// update and the Philox generator of the regrowth draws.
 #pragma once
 
 #include "ffsl_internal.h"
@@ -131,6 +132,32 @@ __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &v
     vv = b2 * vv + (1.f - b2) * g * g;
     const float den = __builtin_amdgcn_sqrtf(vv * inv_bc2) + eps;
     return p - (lr * inv_bc1) * mm * __builtin_amdgcn_rcpf(den);
+}
+
+// Regrowth draws of SET: Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)
+// keyed by (seed, SET_KEY_HI) and counted by (row, set_round, attempt / 4, 0).
+constexpr uint64_t SET_KEY_HI = 0x5345545F52454752ull;  // "SET_REGR"
+
+// Philox4x64-10 round structure: two 64x64->128 multiplies per round, the
+// high halves mixed with the other counter words and the round key, the key
+// advanced by the Weyl increments (golden ratio, sqrt(3)-1) between rounds.
+__device__ __forceinline__ void philox4x64_10(uint64_t &c0, uint64_t &c1, uint64_t &c2,
+                                              uint64_t &c3, uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        const uint64_t n0 = hi1 ^ c1 ^ k0;
+        const uint64_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
 }
 
 }  // namespace fdev

@@ -79,14 +79,31 @@ struct MxArgs {
     // passes in dwp [L][32], dbp [L]
     int32_t b0, Btot;
     float *dwp, *dbp;
+    // SET fused into the pass that applies Adam (see the SETF kernels)
+    int32_t set_n, set_cap;
+    uint64_t set_seed, set_round;
+    uint8_t *set_mask;
+    int32_t *set_exhausted;
+    uint32_t nb_mask;
 };
 
 // pass roles (see launch_sweep_mx)
 constexpr int MX_ONLY = PASS_ONLY, MX_FIRST = PASS_FIRST, MX_LAST = PASS_LAST, MX_MIDDLE = PASS_MIDDLE;
 
 struct Rsrcs {
-    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp;
+    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp, mk;
 };
+
+constexpr int MX_SET_NMAX = 8;   // pruned slots per row the fused SET handles
+constexpr int MX_SET_AHEAD = 8;  // chunks whose first candidates a wave draws at once
+
+// minimum of x over the 16 lanes of a DPP row, in every lane
+__device__ __forceinline__ uint32_t min16(uint32_t x) {
+    x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, DPP_ROW_MIRROR, 0xf, 0xf, false));
+    x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, DPP_ROW_HALF_MIRROR, 0xf, 0xf, false));
+    x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, DPP_QUAD_3210, 0xf, 0xf, false));
+    return min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, DPP_QUAD_1032, 0xf, 0xf, false));
+}
 
 // G and T rows hold 32 bf16 (64 bytes = four 16-byte chunks).  The matrix-
 // core fragments read one chunk from each of 16 consecutive rows; stored
@@ -130,7 +147,9 @@ __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_
 
 // NT = column tiles of 16 per wave: d = 128 * NT (a compile-time width keeps
 // the dX accumulators in fixed registers)
-template <int NT, int MODE>
+// SETF: this pass applies Adam and then SET prune-and-regrow to every row
+// (only with MODE MX_ONLY or MX_LAST)
+template <int NT, int MODE, bool SETF>
 __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     constexpr bool ADAM = MODE == MX_ONLY || MODE == MX_LAST;      // updates W, m, v, bias
     constexpr bool CARRY_IN = MODE == MX_LAST || MODE == MX_MIDDLE;
@@ -143,6 +162,9 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     uint32_t *Ws = reinterpret_cast<uint32_t *>(Is + MX_NLAB * MX_K);      // 32 * 16
     uint32_t *tg = Ws + MX_NLAB * (MX_K / 2);                              // MX_TG_MAX
     uint32_t *ym = tg;   // [32][2]: only when the positives do not fit in tg
+    // SETF: the first four regrowth candidates of each wave's rows of the next
+    // MX_SET_AHEAD chunks, [wave][chunk][row][4] u16
+    uint16_t *Pc = reinterpret_cast<uint16_t *>(tg + MX_TG_MAX);
 
     const int tid = threadIdx.x;
     const int lab = tid >> 4, u = tid & 15;
@@ -166,6 +188,7 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     R.bv = make_rsrc(a.bv, a.nb_b);
     R.dwp = make_rsrc(a.dwp, MODE == MX_ONLY ? 0u : a.nb_m);
     R.dbp = make_rsrc(a.dbp, MODE == MX_ONLY ? 0u : a.nb_b);
+    R.mk = make_rsrc(a.set_mask, SETF ? a.nb_mask : 0u);
 
     Prefetch pa, pb;
     prefetch<ADAM>(a, R, blockIdx.x, tid, lab, u, Kown, pa);
@@ -245,6 +268,23 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     auto step = [&](int64_t chunk, const Prefetch &cur, Prefetch &nxt) {
         const int64_t l0 = chunk * MX_NLAB;
         const uint32_t l0u = (uint32_t)l0;   // L < 2^25: label offsets fit in 32 bits
+        // this workgroup's chunk count so far
+        const int ci = (int)((chunk - blockIdx.x) / gridDim.x);
+        if constexpr (SETF) {
+            // Every MX_SET_AHEAD chunks a wave draws the first Philox block of
+            // its rows in the next MX_SET_AHEAD chunks, one row per lane (each
+            // row's 16 lanes would otherwise all draw the same block), and
+            // keeps the four candidate columns.
+            if ((ci & (MX_SET_AHEAD - 1)) == 0 && lane < 4 * MX_SET_AHEAD) {
+                const int64_t lr = (chunk + (int64_t)(lane >> 2) * gridDim.x) * MX_NLAB + 4 * wave + (lane & 3);
+                uint64_t p0 = (uint64_t)lr, p1 = a.set_round, p2 = 0, p3 = 0;
+                philox4x64_10(p0, p1, p2, p3, a.set_seed, SET_KEY_HI);
+                typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+                const u16x4 cw = {(uint16_t)__umul64hi(p0, (uint64_t)d), (uint16_t)__umul64hi(p1, (uint64_t)d),
+                                  (uint16_t)__umul64hi(p2, (uint64_t)d), (uint16_t)__umul64hi(p3, (uint64_t)d)};
+                *reinterpret_cast<u16x4 *>(Pc + (wave * 4 * MX_SET_AHEAD + lane) * 4) = cw;
+            }
+        }
 
         // stage this chunk's rows: indices become clamped byte offsets of X columns
         {
@@ -391,9 +431,97 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 const float n0 = adam_step(w0, dw0, m0, v0, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
                 const float n1 = adam_step(w1, dw1, m1, v1, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
                 const uint32_t o = (uint32_t)(l * MX_K + Kown);
+                uint32_t wnew = pack_bf16(n0, n1);
+                if constexpr (SETF) {
+                    // SET on the updated row (Sec. 2.1): the n slots with the
+                    // smallest keys (|W| bits, slot) of the stored bf16 weights.
+                    // Every lane of the row finds the same slots: n rounds of a
+                    // row-wide minimum, the owner of each minimum dropping it.
+                    const uint32_t k0 = ((wnew & 0x7fffu) << 5) | (uint32_t)Kown;
+                    const uint32_t k1 = (((wnew >> 16) & 0x7fffu) << 5) | (uint32_t)(Kown + 1);
+                    uint32_t klo = min(k0, k1), khi = max(k0, k1);
+                    uint32_t sel = 0;   // the row's pruned slots
+                    for (int q = 0; q < a.set_n; ++q) {
+                        const uint32_t mn = min16(klo);
+                        sel |= 1u << (mn & 31u);
+                        if (klo == mn) {
+                            klo = khi;
+                            khi = 0xffffffffu;
+                        }
+                    }
+                    // Regrowth: attempt t takes word t mod 4 of Philox4x64-10 at
+                    // counter (row, round, t / 4, 0); a column the row held
+                    // before pruning or one already accepted is drawn again.
+                    // Lane j of the row keeps the j-th accepted column, so one
+                    // ballot over the row's lanes answers both questions.
+                    int acol = -1;
+                    int got = 0;
+                    const int rsh = 16 * (lab & 3);   // this row's lanes in a wave-wide ballot
+                    auto offer = [&](int c) {
+                        const uint64_t held = __builtin_amdgcn_ballot_w64(c == c0 || c == c1 || c == acol);
+                        if (((held >> rsh) & 0xffffull) == 0) {
+                            if (u == got) acol = c;
+                            ++got;
+                        }
+                    };
+                    // attempts 0-3: the candidates drawn ahead
+                    {
+                        typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+                        const u16x4 cw = *reinterpret_cast<const u16x4 *>(
+                            Pc + (wave * 4 * MX_SET_AHEAD + 4 * (ci & (MX_SET_AHEAD - 1)) + (lab & 3)) * 4);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            if (got < a.set_n) offer((int)cw[q]);
+                    }
+                    // later attempts (a row that met a held column): drawn here
+                    uint64_t p0 = 0, p1 = 0, p2 = 0, p3 = 0;
+                    for (int att = 4; got < a.set_n && att < a.set_cap; ++att) {
+                        if ((att & 3) == 0) {
+                            p0 = (uint64_t)l;
+                            p1 = a.set_round;
+                            p2 = (uint64_t)(att >> 2);
+                            p3 = 0;
+                            philox4x64_10(p0, p1, p2, p3, a.set_seed, SET_KEY_HI);
+                        }
+                        const int ws = att & 3;
+                        const uint64_t word = ws == 0 ? p0 : ws == 1 ? p1 : ws == 2 ? p2 : p3;
+                        offer((int)__umul64hi(word, (uint64_t)d));
+                    }
+                    // a row that ran out of attempts keeps its slots
+                    if (got < a.set_n) {
+                        sel = 0;
+                        if (valid && u == 0 && a.set_exhausted) atomicAdd(a.set_exhausted, 1);
+                    }
+                    // pruned slots restart at zero
+                    if ((sel >> Kown) & 1u) {
+                        wnew &= 0xffff0000u;
+                        m0 = v0 = 0.f;
+                    }
+                    if ((sel >> (Kown + 1)) & 1u) {
+                        wnew &= 0x0000ffffu;
+                        m1 = v1 = 0.f;
+                    }
+                    // the row's index words (this lane's load: slots 2u, 2u+1),
+                    // rewritten whole: the regrown columns fill the pruned
+                    // slots in ascending slot order, the others keep their bits
+                    const int s0 = 2 * u, s1 = 2 * u + 1;
+                    const int r0 = __builtin_popcount(sel & ((1u << s0) - 1u));
+                    const int r1 = r0 + (int)((sel >> s0) & 1u);
+                    const int rowlane = lane & ~15;   // lane 0 of this row in the wave
+                    const uint32_t n0c = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * (rowlane + min(r0, 15)), acol);
+                    const uint32_t n1c = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * (rowlane + min(r1, 15)), acol);
+                    const uint32_t iw0 = ((sel >> s0) & 1u) ? n0c : cur.iv.x;
+                    const uint32_t iw1 = ((sel >> s1) & 1u) ? n1c : cur.iv.y;
+                    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                    const u32x2 iw = {iw0, iw1};
+                    const uint32_t oi = valid ? (uint32_t)(l * MX_K + s0) * 4u : a.nb_I;
+                    __builtin_amdgcn_raw_buffer_store_b64(iw, R.I, oi, 0, 0);
+                    const uint16_t mk = (uint16_t)(((sel >> s0) & 1u) | (((sel >> s1) & 1u) << 8));
+                    __builtin_amdgcn_raw_buffer_store_b16(mk, R.mk, valid ? (uint32_t)(l * MX_K + s0) : a.nb_mask, 0, 0);
+                }
                 stf2(R.m, valid ? 4u * o : a.nb_m, make_float2(m0, m1));
                 stf2(R.v, valid ? 4u * o : a.nb_m, make_float2(v0, v1));
-                st32(R.W, valid ? 2u * o : a.nb_W, pack_bf16(n0, n1));
+                st32(R.W, valid ? 2u * o : a.nb_W, wnew);
             }
             // bias: sum of g over the 64 rows, lane u == 0 updates
             {
@@ -483,23 +611,26 @@ constexpr int MX_NT_MAX = 6;    // widest input: 768 columns
 typedef void (*MxKernel)(const MxArgs);
 template <int NT>
 struct MxModes {
-    static constexpr MxKernel k[4] = {k_sweep_mx<NT, MX_ONLY>, k_sweep_mx<NT, MX_FIRST>, k_sweep_mx<NT, MX_LAST>,
-                                      k_sweep_mx<NT, MX_MIDDLE>};
+    static constexpr MxKernel k[4] = {k_sweep_mx<NT, MX_ONLY, false>, k_sweep_mx<NT, MX_FIRST, false>,
+                                      k_sweep_mx<NT, MX_LAST, false>, k_sweep_mx<NT, MX_MIDDLE, false>};
+    // the passes that apply Adam, with SET fused
+    static constexpr MxKernel kset[4] = {k_sweep_mx<NT, MX_ONLY, true>, nullptr, k_sweep_mx<NT, MX_LAST, true>,
+                                         nullptr};
 };
-MxKernel mx_kernel(int nt, int mode) {
+MxKernel mx_kernel(int nt, int mode, bool setf) {
     switch (nt) {
-    case 1: return MxModes<1>::k[mode];
-    case 2: return MxModes<2>::k[mode];
-    case 3: return MxModes<3>::k[mode];
-    case 4: return MxModes<4>::k[mode];
-    case 5: return MxModes<5>::k[mode];
-    default: return MxModes<6>::k[mode];
+    case 1: return setf ? MxModes<1>::kset[mode] : MxModes<1>::k[mode];
+    case 2: return setf ? MxModes<2>::kset[mode] : MxModes<2>::k[mode];
+    case 3: return setf ? MxModes<3>::kset[mode] : MxModes<3>::k[mode];
+    case 4: return setf ? MxModes<4>::kset[mode] : MxModes<4>::k[mode];
+    case 5: return setf ? MxModes<5>::kset[mode] : MxModes<5>::k[mode];
+    default: return setf ? MxModes<6>::kset[mode] : MxModes<6>::k[mode];
     }
 }
 
-size_t sweep_mx_lds(int d) {
+size_t sweep_mx_lds(int d, bool setf = false) {
     return (size_t)d * MX_XS + (size_t)d * MX_NLAB * 2 + MX_NB * MX_NLAB * 2 + MX_NLAB * MX_K * 4 +
-           MX_NLAB * (MX_K / 2) * 4 + MX_TG_MAX * 4;
+           MX_NLAB * (MX_K / 2) * 4 + MX_TG_MAX * 4 + (setf ? (MX_THREADS / 64) * 4 * MX_SET_AHEAD * 8 : 0);
 }
 
 }  // namespace
@@ -509,6 +640,8 @@ bool sweep_mx_eligible(const Layer &ly, int B, int mode) {
            ly.d >= 128 && ly.d <= 128 * MX_NT_MAX && ly.L < ((int64_t)1 << 25) && sweep_mx_lds(ly.d) <= 160 * 1024;
 }
 
+// With c.set_n in [1, MX_SET_NMAX] the pass that applies Adam also applies
+// SET to every row (the SETF kernels).
 // Batches of up to 64 samples take one pass.  A larger batch is split into
 // passes of 64 samples: every pass accumulates its samples' dX rows and loss,
 // the first stores its dW / dbias in the carry buffers, middle passes add to
@@ -538,12 +671,19 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.dwp = dwp;
     a.dbp = dbp;
     a.Btot = c.B;
+    const bool setf = c.set_n >= 1 && c.set_n <= MX_SET_NMAX && sweep_mx_lds(ly.d, true) <= 160 * 1024;
+    a.set_n = c.set_n;
+    a.set_cap = 64 * MX_K + 4096;
+    a.set_seed = c.set_seed;
+    a.set_round = c.set_round;
+    a.set_mask = c.set_mask;
+    a.set_exhausted = c.set_exhausted;
+    a.nb_mask = c.set_mask ? (uint32_t)(ly.L * MX_K) : 0u;
     a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * MX_K * 2);
     a.nb_I = (uint32_t)(ly.L * MX_K * 4);
     a.nb_m = (uint32_t)(ly.L * MX_K * 4);
     a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
-    const size_t shm = sweep_mx_lds(ly.d);
     const int grid = (int)std::min<int64_t>(a.nchunks, std::min(ly.max_parts, ly.num_cu));
     const int passes = (c.B + MX_NB - 1) / MX_NB;
     if (ly.ev_start) {
@@ -555,7 +695,9 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
         a.b0 = p * MX_NB;
         a.B = std::min(MX_NB, c.B - a.b0);
         a.loss_part = loss_part + (size_t)p * grid;
-        const MxKernel kern = mx_kernel(ly.d / 128, mode);
+        const bool kset = setf && (mode == MX_ONLY || mode == MX_LAST);
+        const MxKernel kern = mx_kernel(ly.d / 128, mode, kset);
+        const size_t shm = sweep_mx_lds(ly.d, kset);
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
@@ -569,6 +711,7 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     }
     *grid_out = grid;
     *passes_out = passes;
+    if (setf && c.set_fused) *c.set_fused = true;
     return FFSL_OK;
 }
 

@@ -33,6 +33,8 @@ SIGNATURES = {
     "ffsl_adam_step": (_int, [_vp, _i64, _f32, _f32, _f32, _f32, _f32, _vp]),
     "ffsl_train_step": (_int, [_vp, _vp, _i32, _vp, _vp, _i32, _f32, _i64, _f32, _f32, _f32, _f32,
                                _f32, _vp, _vp, _u32, _vp]),
+    "ffsl_train_step_set": (_int, [_vp, _vp, _i32, _vp, _vp, _i32, _f32, _i64, _f32, _f32, _f32, _f32,
+                                   _f32, _vp, _vp, _u32, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_set_update": (_int, [_vp, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_validate_indices": (_int, [_vp, _vp, _vp]),
     "ffsl_set_timing_events": (_int, [_vp, _vp, _vp]),
@@ -221,6 +223,28 @@ class SparseLayer:
                                       lr, beta1, beta2, eps, wd, _ptr(loss), _ptr(dX), flags,
                                       _stream(torch)))
         return loss, dX
+
+    def train_step_set(self, X, off, lab, t, frac, seed, set_round, s=None, lr=1e-3, beta1=0.9,
+                       beta2=0.999, eps=1e-8, wd=0.0, loss_out=None, dX_out=None, want_dx=True, flags=0,
+                       mask=True, exhausted_out=None):
+        """train_step followed by set_update, fused where the library can."""
+        torch = self.torch
+        X, off, lab, nnz = self._batch(X, off, lab)
+        B = X.shape[0]
+        s = 1.0 / B if s is None else float(s)
+        loss = loss_out if loss_out is not None else torch.empty(1, dtype=torch.float32, device=X.device)
+        dX = dX_out
+        if dX is None and want_dx:
+            dX = torch.empty((B, self.d), dtype=torch.float32, device=X.device)
+        msk = torch.empty((self.L, self.k), dtype=torch.uint8, device=self.W.device) if mask else None
+        ex = exhausted_out
+        if ex is None:
+            ex = torch.zeros(1, dtype=torch.int32, device=self.W.device)
+        _check(load().ffsl_train_step_set(self._handle, _ptr(X), B, _ptr(off), _ptr(lab), nnz, s, int(t),
+                                          lr, beta1, beta2, eps, wd, _ptr(loss), _ptr(dX), flags,
+                                          float(frac), int(seed) & (2**64 - 1), int(set_round) & (2**64 - 1),
+                                          _ptr(msk), _ptr(ex), _stream(torch)))
+        return loss, dX, msk, ex
 
     def set_update(self, frac, seed, set_round, mask=True, exhausted_out=None):
         torch = self.torch
