@@ -45,6 +45,8 @@ def lib():
         L.ffslref_targets_dense.restype = None
         L.ffslref_bce.argtypes = [i64, vp, vp, dbl, vp]
         L.ffslref_bce.restype = dbl
+        L.ffslref_sqhinge.argtypes = [i64, vp, vp, dbl, vp]
+        L.ffslref_sqhinge.restype = dbl
         L.ffslref_backward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
         L.ffslref_backward.restype = None
         L.ffslref_adam.argtypes = [i64, vp, vp, vp, vp, i64, dbl, dbl, dbl, dbl, dbl]
@@ -133,6 +135,18 @@ def bce(z, y, s):
     return loss, g
 
 
+def sqhinge(z, y, s):
+    """Returns (loss, g) for the squared hinge loss summed and scaled by s."""
+    z = _f64(z)
+    y = np.ascontiguousarray(y, dtype=np.uint8)
+    g = np.empty_like(z)
+    loss = lib().ffslref_sqhinge(z.size, _p(z), _p(y), float(s), _p(g))
+    return loss, g
+
+
+LOSSES = {"bce": bce, "sqhinge": sqhinge}
+
+
 def backward(X, W, I, g, want_dbias=True, want_dx=True):
     X, W, I, g = _f64(X), _f64(W), _i32(I), _f64(g)
     B, d = X.shape
@@ -151,27 +165,29 @@ def adam(p, m, v, grad, t, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, wd=0.0):
     return p, m, v
 
 
-def loss_and_grads(X, W, I, bias, off, lab, s):
-    """Forward, BCE and both backward products for one batch."""
+def loss_and_grads(X, W, I, bias, off, lab, s, loss="bce"):
+    """Forward, the loss (BCE or squared hinge) and both backward products for
+    one batch."""
     B = X.shape[0]
     L = W.shape[0]
     z = forward(X, W, I, bias)
     y = targets_dense(B, L, off, lab)
-    loss, g = bce(z, y, s)
+    loss, g = LOSSES[loss](z, y, s)
     dW, dbias, dX = backward(X, W, I, g)
     return dict(z=z, y=y, loss=loss, g=g, dW=dW, dbias=dbias, dX=dX)
 
 
 def train_step(X, W, I, bias, m, v, bm, bv, off, lab, s, t, lr=1e-3, b1=0.9,
-               b2=0.999, eps=1e-8, wd=0.0, w_bf16=False):
-    """One step of the method on the sparse layer: forward, BCE, backward, Adam.
+               b2=0.999, eps=1e-8, wd=0.0, w_bf16=False, loss="bce"):
+    """One step of the method on the sparse layer: forward, loss (BCE or squared
+    hinge), backward, Adam.
 
     W is float64 (the stored values widened).  With ``w_bf16`` the updated
     weights are rounded to bf16 as a bf16-stored weight would be; the result
     ``W`` is then float64 of those bf16 values.  Returns a dict with the new
     state, the loss and dX.
     """
-    r = loss_and_grads(X, W, I, bias, off, lab, s)
+    r = loss_and_grads(X, W, I, bias, off, lab, s, loss=loss)
     Wn, mn, vn = adam(W, m, v, r["dW"], t, lr, b1, b2, eps, wd)
     if w_bf16:
         Wn = bf16_to_f64(round_bf16(Wn))

@@ -19,6 +19,7 @@
  * Parity status of each function (what pins it in tests/test_oracle_*.py):
  *   forward / backward   dense masked matmul + autograd + finite differences
  *   bce                  closed form + torch BCE-with-logits
+ *   sqhinge              hand-computed values, finite differences, symmetry
  *   adam                 torch.optim.Adam / AdamW
  *   round_bf16           torch float32 -> bfloat16 conversion
  *   philox4x64_10        numpy.random.Philox (a library implementation)
@@ -84,6 +85,28 @@ EXPORT double ffslref_bce(int64_t n, const double *z, const uint8_t *y, double s
             double sig = 1.0 / (1.0 + exp(-zz));
             g[t] = s * (sig - yy);
         }
+    }
+    return s * loss;
+}
+
+/* Squared hinge loss (the loss of every dataset but LF-AmazonTitles-131K,
+ * Appendix "Hyperparameter Settings"; the paper names it without a formula,
+ * so we take the textbook one), with signed targets yh = 2y - 1, summed and
+ * scaled by s:
+ *     loss = s * sum_n max(0, 1 - yh_n z_n)^2
+ *     g_n  = d loss / d z_n = -2 s yh_n max(0, 1 - yh_n z_n).
+ * g_n is exactly 0 wherever yh_n z_n >= 1: the activation sparsity that Sec.
+ * 2.2 counts on for the backward pass.                                      */
+EXPORT double ffslref_sqhinge(int64_t n, const double *z, const uint8_t *y, double s,
+                              double *g)
+{
+    double loss = 0.0;
+    for (int64_t t = 0; t < n; ++t) {
+        double yh = y[t] ? 1.0 : -1.0;
+        double h = 1.0 - yh * z[t];
+        if (h < 0.0) h = 0.0;
+        loss += h * h;
+        if (g) g[t] = -2.0 * s * yh * h;
     }
     return s * loss;
 }

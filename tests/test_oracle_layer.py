@@ -99,6 +99,72 @@ def test_bce_matches_torch(oracle):
     np.testing.assert_allclose(g, zt.grad.numpy(), rtol=1e-12, atol=1e-15)
 
 
+# ------------------------------------------------------- squared hinge
+
+def test_sqhinge_hand_values(oracle):
+    """Per-element values worked out from max(0, 1 - yh z)^2 with yh = 2y - 1."""
+    z = np.array([0.0, 0.0, 2.0, -3.0, 0.5, -0.5, 1.0, -1.0, 1.5, -7.0])
+    y = np.array([0, 1, 1, 0, 1, 0, 1, 0, 0, 1], dtype=np.uint8)
+    s = 0.125
+    loss, g = oracle.sqhinge(z, y, s)
+    # hinge h = 1 - yh z: 1, 1, -1, -2, 0.5, 0.5, 0, 0, 2.5, 8
+    assert loss == s * (1 + 1 + 0 + 0 + 0.25 + 0.25 + 0 + 0 + 6.25 + 64)
+    np.testing.assert_array_equal(g, s * np.array([2.0, -2.0, 0, 0, -1.0, 1.0, 0, 0, 5.0, -16.0]))
+
+
+def test_sqhinge_gradient_by_central_differences(oracle):
+    rng = np.random.default_rng(5)
+    z = rng.standard_normal(200) * 2
+    y = (rng.random(200) < 0.3).astype(np.uint8)
+    keep = np.abs(1 - (2.0 * y - 1.0) * z) > 1e-3     # away from the kink
+    z, y = z[keep], y[keep]
+    _, g = oracle.sqhinge(z, y, 0.5)
+    h = 1e-6
+    for i in range(0, len(z), 7):
+        zp, zm = z.copy(), z.copy()
+        zp[i] += h
+        zm[i] -= h
+        fd = (oracle.sqhinge(zp, y, 0.5)[0] - oracle.sqhinge(zm, y, 0.5)[0]) / (2 * h)
+        np.testing.assert_allclose(g[i], fd, rtol=1e-6, atol=1e-9)
+
+
+def test_sqhinge_symmetry_and_sparsity(oracle):
+    rng = np.random.default_rng(6)
+    z = rng.standard_normal(500) * 3
+    ones, zeros = np.ones(500, np.uint8), np.zeros(500, np.uint8)
+    l1, g1 = oracle.sqhinge(z, ones, 1.0)
+    l0, g0 = oracle.sqhinge(-z, zeros, 1.0)
+    assert l1 == l0
+    np.testing.assert_array_equal(g1, -g0)
+    # exactly zero gradient where the margin holds (yh z >= 1), nonzero elsewhere
+    assert np.all(g1[z >= 1] == 0) and np.all(g1[z < 1] != 0)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_sqhinge_backward_matches_autograd_of_dense_masked_layer(oracle, seed):
+    """The sparse layer's gradients under the squared hinge against autograd of
+    the dense masked layer (the loss written with torch ops)."""
+    X, W, I, b, off, lab = tiny_case(seed, B=6, d=13, L=10, k=5)
+    s = 1 / 6
+    r = oracle.loss_and_grads(X, W, I, b, off, lab, s, loss="sqhinge")
+    B, d = X.shape
+    L, k = W.shape
+    y = np.zeros((B, L))
+    for bb in range(B):
+        y[bb, lab[off[bb]:off[bb + 1]]] = 1
+    Xt = torch.tensor(X, requires_grad=True)
+    Mt = torch.tensor(dense_mask(W, I, d), requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    zt = Xt @ Mt.T + bt
+    yh = torch.tensor(2 * y - 1)
+    loss = (torch.clamp(1 - yh * zt, min=0) ** 2).sum() * s
+    loss.backward()
+    np.testing.assert_allclose(r["loss"], loss.item(), rtol=1e-13)
+    np.testing.assert_allclose(r["dW"], Mt.grad.numpy()[np.arange(L)[:, None], I], rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(r["dbias"], bt.grad.numpy(), rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(r["dX"], Xt.grad.numpy(), rtol=1e-11, atol=1e-14)
+
+
 # -------------------------------------------------------------- gradients
 
 def torch_dense_reference(X, W, I, b, off, lab, s):
