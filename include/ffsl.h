@@ -56,6 +56,15 @@ typedef enum {
 /* flags */
 #define FFSL_ACCUM_DX 1u   /* add into dX_out instead of overwriting it      */
 #define FFSL_ACCUM_LOSS 2u /* add into *loss_out instead of overwriting it   */
+/* The sparse layer's loss is the squared hinge instead of BCE (the loss the
+ * paper trains every dataset but LF-AmazonTitles-131K with, Appendix
+ * "Hyperparameter Settings"), with signed targets yh = 2y - 1:
+ *   loss = s * sum_{b,l} max(0, 1 - yh z)^2,   g = -2 s yh max(0, 1 - yh z).
+ * g is exactly zero where yh z >= 1 (Sec. 2.2: the activation sparsity of a
+ * hinge-like loss); the fused paths skip the dW products of a wave whose
+ * dlogits are all zero.  Accepted by ffsl_forward_loss, ffsl_backward,
+ * ffsl_train_step and ffsl_train_step_set. */
+#define FFSL_LOSS_SQHINGE 4u
 
 /* Limits of this build. */
 #define FFSL_MAX_K 128         /* fan-in                                    */
@@ -106,7 +115,7 @@ FFSL_API int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k
 FFSL_API int ffsl_destroy_layer(ffsl_layer *layer);
 
 /* Gathered forward and BCE loss (Sec. 2.2; Appendix "Hyperparameter
- * Settings"):
+ * Settings"; the squared hinge with FFSL_LOSS_SQHINGE):
  *   z[b,l]  = bias[l] + sum_j W[l,j] * X[b, I[l,j]]
  *   *loss_out (device fp32) = s * sum_{b,l} [max(z,0) - z*y + log1p(exp(-|z|))]
  * with y[b,l] = 1 iff l is a positive of sample b.
@@ -124,9 +133,9 @@ FFSL_API int ffsl_forward_loss(ffsl_layer *layer, const void *X, int32_t B,
                       int32_t nnz, float s, float *loss_out, float *logits_out,
                       uint32_t flags, void *stream);
 
-/* Both backward products (Sec. 2.2) of the BCE loss above, recomputing the
+/* Both backward products (Sec. 2.2) of the loss above, recomputing the
  * scores in the same sweep:
- *   g[b,l]   = s * (sigmoid(z[b,l]) - y[b,l])
+ *   g[b,l]   = s * (sigmoid(z[b,l]) - y[b,l])   (squared hinge: see the flag)
  *   dW[l,j]  = sum_b g[b,l] * X[b, I[l,j]]      -> layer dW  (fp32 [L,k])
  *   dbias[l] = sum_b g[b,l]                     -> layer dbias (if bias)
  *   dX[b,i]  = sum_{l,j: I[l,j]=i} g[b,l]*W[l,j] -> dX_out fp32 [B,d]

@@ -41,6 +41,7 @@ struct SweepArgs {
     float *loss_part;
     float *dx_part;
     int want_loss;
+    int hinge;   // squared hinge instead of BCE
 };
 
 template <int KM>
@@ -211,14 +212,17 @@ __global__ void __launch_bounds__(SW_THREADS) k_sweep(const SweepArgs a) {
                         }
                     }
                     const float y = ((ym[tid * YM_WORDS + (bb >> 5)] >> (bb & 31)) & 1u) ? 1.f : 0.f;
-                    const float e = expf(-fabsf(z));
+                    // BCE with logits, or the squared hinge with yh = 2y - 1
+                    const float yh = 2.f * y - 1.f;
+                    const float hh = fmaxf(1.f - yh * z, 0.f);
+                    const float e = a.hinge ? 0.f : expf(-fabsf(z));
                     if (MODE != SWEEP_BWD || a.want_loss)
-                        loss_acc += fmaxf(z, 0.f) - z * y + log1pf(e);
+                        loss_acc += a.hinge ? hh * hh : fmaxf(z, 0.f) - z * y + log1pf(e);
                     if (MODE == SWEEP_FWD && a.logits) a.logits[(int64_t)(b0 + bb) * a.L + l] = z;
                     if (MODE != SWEEP_FWD) {
                         const float r = 1.f / (1.f + e);
                         const float sig = z >= 0.f ? r : e * r;
-                        const float g = a.s * (sig - y);
+                        const float g = a.hinge ? -2.f * a.s * yh * hh : a.s * (sig - y);
                         db += g;
                         float *dxr = dXs + (size_t)bb * d;
 #pragma unroll
@@ -427,6 +431,7 @@ int launch_sweep(const SweepCall &c) {
     a.loss_part = reinterpret_cast<float *>(ly.ws + wl.loss_part);
     a.dx_part = reinterpret_cast<float *>(ly.ws + wl.dx_part);
     a.want_loss = c.loss_out != nullptr;
+    a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
 
     int grid = (int)std::min<int64_t>(a.nchunks, ly.max_parts);
 

@@ -79,6 +79,7 @@ struct MxArgs {
     // passes in dwp [L][32], dbp [L]
     int32_t b0, Btot;
     float *dwp, *dbp;
+    int32_t hinge;   // squared hinge instead of BCE
     // SET fused into the pass that applies Adam (see the SETF kernels)
     int32_t set_n, set_cap;
     uint64_t set_seed, set_round;
@@ -395,33 +396,39 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 const bool live = valid && 4 * u + e < a.B;
                 const float zz = z[e] + cur.b;
                 const float y = ((yw >> e) & 1u) ? 1.f : 0.f;
-                // exp(-|z|) in (0, 1] and log(1 + exp(-|z|)) with the hardware
-                // base-2 exp and log (their arguments need no range reduction)
-                const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
-                const float opx = 1.f + ex;
-                const float r = __builtin_amdgcn_rcpf(opx);
-                const float sig = zz >= 0.f ? r : ex * r;
-                loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
-                                 : 0.f;
-                g[e] = live ? a.s * (sig - y) : 0.f;
+                if (a.hinge) {
+                    // squared hinge with yh = 2y - 1
+                    const float yh = 2.f * y - 1.f;
+                    const float hh = fmaxf(1.f - yh * zz, 0.f);
+                    loss_acc += live ? hh * hh : 0.f;
+                    g[e] = live ? -2.f * a.s * yh * hh : 0.f;
+                } else {
+                    // exp(-|z|) in (0, 1] and log(1 + exp(-|z|)) with the
+                    // hardware base-2 exp and log (their arguments need no
+                    // range reduction)
+                    const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
+                    const float opx = 1.f + ex;
+                    const float r = __builtin_amdgcn_rcpf(opx);
+                    const float sig = zz >= 0.f ? r : ex * r;
+                    loss_acc += live ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
+                                     : 0.f;
+                    g[e] = live ? a.s * (sig - y) : 0.f;
+                }
             }
             // dW partials over the lane's rows, slot order r ^ Kp
             const uint32_t g01 = pack_bf16(g[0], g[1]), g23 = pack_bf16(g[2], g[3]);
-            float pw[MX_K];
+            // a wave whose dlogits are all zero (a hinge loss past its margin
+            // everywhere, Sec. 2.2) has zero dW: its products are skipped
+            float dw0 = dprev.x, dw1 = dprev.y;
+            if (__builtin_amdgcn_ballot_w64((g01 | g23) != 0u) != 0) {
+                float pw[MX_K];
 #pragma unroll
-            for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2z(xg[r].x, g01));
-            // reduce-scatter over the 16 lanes of the row
-#pragma unroll
-            for (int r = 0; r < 16; ++r) pw[r] = add_dpp<DPP_ROW_MIRROR>(pw[r], pw[16 + r]);
-#pragma unroll
-            for (int r = 0; r < 8; ++r) pw[r] = add_dpp<DPP_ROW_HALF_MIRROR>(pw[r], pw[8 + r]);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_3210>(pw[r], pw[4 + r]);
-            // last level: lanes u and u^1 hold the same four slots; both add, each
-            // keeps its two
-#pragma unroll
-            for (int r = 0; r < 4; ++r) pw[r] = add_dpp<DPP_QUAD_1032>(pw[r], pw[r]);
-            const float dw0 = (odd ? pw[2] : pw[0]) + dprev.x, dw1 = (odd ? pw[3] : pw[1]) + dprev.y;
+                for (int r = 0; r < MX_K; ++r) pw[r] = dot2(xg[r].y, g23, dot2z(xg[r].x, g01));
+                // reduce-scatter over the 16 lanes of the row
+                const float2 dws = reduce_scatter16(pw, odd);
+                dw0 += dws.x;
+                dw1 += dws.y;
+            }
             if constexpr (!ADAM) stf2(R.dwp, odw, make_float2(dw0, dw1));
             // Adam on slots Kown, Kown+1
             if constexpr (ADAM) {
@@ -671,6 +678,7 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.dwp = dwp;
     a.dbp = dbp;
     a.Btot = c.B;
+    a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
     const bool setf = c.set_n >= 1 && c.set_n <= MX_SET_NMAX && sweep_mx_lds(ly.d, true) <= 160 * 1024;
     a.set_n = c.set_n;
     a.set_cap = 64 * MX_K + 4096;

@@ -75,6 +75,7 @@ struct WdArgs {
     // passes in dwp [L][64], dbp [L]
     int32_t b0, Btot;
     float *dwp, *dbp;
+    int32_t hinge;   // squared hinge instead of BCE
 };
 
 struct Rsrcs {
@@ -330,24 +331,39 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
         // past L; the loss is counted once, in half 0
         const bool live = valid && bs < a.B;
         const float y = ((yrow >> bs) & 1u) ? 1.f : 0.f;
-        const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
-        const float opx = 1.f + ex;
-        const float rr = __builtin_amdgcn_rcpf(opx);
-        const float sig = zz >= 0.f ? rr : ex * rr;
-        loss_acc += live && h == 0 ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
-                                   : 0.f;
-        const float g = live ? a.s * (sig - y) : 0.f;
+        float g;
+        if (a.hinge) {
+            // squared hinge with yh = 2y - 1
+            const float yh = 2.f * y - 1.f;
+            const float hh = fmaxf(1.f - yh * zz, 0.f);
+            loss_acc += live && h == 0 ? hh * hh : 0.f;
+            g = live ? -2.f * a.s * yh * hh : 0.f;
+        } else {
+            const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
+            const float opx = 1.f + ex;
+            const float rr = __builtin_amdgcn_rcpf(opx);
+            const float sig = zz >= 0.f ? rr : ex * rr;
+            loss_acc += live && h == 0 ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
+                                       : 0.f;
+            g = live ? a.s * (sig - y) : 0.f;
+        }
         // dW partials of the lane's slots, slot order r ^ Kp
         const uint32_t glo = pack_bf16(g, 0.f), ghi = pack_bf16(0.f, g);
-        float pw[32];
+        // a wave whose dlogits are all zero (a hinge loss past its margin
+        // everywhere, Sec. 2.2) has zero dW: its products are skipped
+        float dw0 = dprev.x, dw1 = dprev.y;
+        if (__builtin_amdgcn_ballot_w64(glo != 0u) != 0) {
+            float pw[32];
 #pragma unroll
-        for (int p = 0; p < 16; ++p) {
-            pw[2 * p] = dot2z(xp[p], glo);
-            pw[2 * p + 1] = dot2z(xp[p], ghi);
+            for (int p = 0; p < 16; ++p) {
+                pw[2 * p] = dot2z(xp[p], glo);
+                pw[2 * p + 1] = dot2z(xp[p], ghi);
+            }
+            // reduce-scatter over the pass's 16 samples
+            const float2 dws = reduce_scatter16(pw, odd);
+            dw0 += dws.x;
+            dw1 += dws.y;
         }
-        // reduce-scatter over the pass's 16 samples
-        const float2 dws = reduce_scatter16(pw, odd);
-        const float dw0 = dws.x + dprev.x, dw1 = dws.y + dprev.y;
         if constexpr (!ADAM) stf2(R.dwp, odw, make_float2(dw0, dw1));
         if constexpr (ADAM) {
             float m0 = cur.m.x, m1 = cur.m.y, v0 = cur.v.x, v1 = cur.v.y;
@@ -492,6 +508,7 @@ int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part
     a.dwp = dwp;
     a.dbp = dbp;
     a.Btot = c.B;
+    a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
     a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * WD_K * 2);
     a.nb_I = (uint32_t)(ly.L * WD_K * 4);

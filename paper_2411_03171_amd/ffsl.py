@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libffsl.so")
 
 FFSL_OK, FFSL_EINVAL, FFSL_EUNSUPPORTED, FFSL_EHIP = 0, -1, -2, -3
 FFSL_F32, FFSL_BF16 = 0, 1
-FFSL_ACCUM_DX, FFSL_ACCUM_LOSS = 1, 2
+FFSL_ACCUM_DX, FFSL_ACCUM_LOSS, FFSL_LOSS_SQHINGE = 1, 2, 4
 
 # (name, restype, argtypes) for every entry point of include/ffsl.h
 _i32, _i64, _u32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
