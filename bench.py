@@ -241,11 +241,14 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="c4_bf16_L3M")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--set-reps", type=int, default=10)
     ap.add_argument("--dense-reps", type=int, default=20)
+    ap.add_argument("--hinge-reps", type=int, default=10,
+                    help="squared hinge steps per case (0 skips them, e.g. under a kernel trace "
+                         "whose per-kernel average should cover the BCE step only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sparse-only", action="store_true",
                     help="for a workload with dense parts, time its sparse layer alone (at the "
@@ -384,6 +387,26 @@ def main():
     print("[bench] step with SET in one call: %.3f ms median (plain step %.3f ms): SET adds %.3f ms" %
           (fused_med, plain_med, fused_med - plain_med), file=sys.stderr, flush=True)
 
+    # the squared hinge (same step, other loss): scores near zero give a
+    # dlogit everywhere; a bias of -4 puts every label without a positive in
+    # the batch past the margin, so waves with no positive skip their dW work
+    hinge = {"dense_dlogits": None, "past_margin": None}
+    bias_saved = layer.bias.clone()
+    for case, fill in (("dense_dlogits", None), ("past_margin", -4.0)) if args.hinge_reps > 0 else ():
+        if fill is not None:
+            layer.bias.fill_(fill)
+        hm = []
+        for r in range(args.hinge_reps):
+            t += 1
+            hm.append(one_step(lambda: layer.train_step(X, off, lab, t=t, loss_out=loss, dX_out=dX,
+                                                        flags=ffsl.FFSL_LOSS_SQHINGE)))
+        hinge[case] = sorted(hm)[len(hm) // 2]
+    layer.bias.copy_(bias_saved)
+    torch.cuda.synchronize()
+    if args.hinge_reps > 0:
+        print("[bench] squared hinge step: %.3f ms (dense dlogits), %.3f ms (past the margin); BCE %.3f ms" %
+              (hinge["dense_dlogits"], hinge["past_margin"], plain_med), file=sys.stderr, flush=True)
+
     dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
@@ -438,6 +461,12 @@ def main():
             "plain_step_ms_median": plain_med,
             "marginal_ms": fused_med - plain_med,
             "note": "ffsl_train_step_set: SET applied in the sweep that applies Adam",
+        },
+        "sqhinge_step": {
+            "ms_median_dense_dlogits": hinge["dense_dlogits"],
+            "ms_median_past_margin": hinge["past_margin"],
+            "bce_step_ms_median": plain_med,
+            "note": "FFSL_LOSS_SQHINGE; past_margin: bias -4, dW work skipped where a wave has no dlogit",
         },
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],
