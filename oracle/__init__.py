@@ -68,6 +68,10 @@ def lib():
         L.ffslref_dense_gelu_bwd.restype = None
         L.ffslref_aux_bce.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, dbl, vp, vp, vp, vp]
         L.ffslref_aux_bce.restype = dbl
+        L.ffslref_topk.argtypes = [i64, i64, vp, i64, vp, vp]
+        L.ffslref_topk.restype = None
+        L.ffslref_precision_at_k.argtypes = [i64, i64, vp, vp, vp, vp]
+        L.ffslref_precision_at_k.restype = None
         _lib = L
     return _lib
 
@@ -277,3 +281,37 @@ def aux_bce(X, Wa, ca, off, lab, s):
     loss = lib().ffslref_aux_bce(B, d, C, _p(X), _p(Wa), _p(cc), _p(off), _p(lab), float(s),
                                  _p(Za), _p(dWa), _p(dca), _p(dXa))
     return dict(loss=loss, Za=Za, dWa=dWa, dca=dca, dXa=dXa)
+
+
+# --------------------------------------------------------------------------
+# inference
+
+def topk(z, K):
+    """Top-K labels of each row of the scores z [B,L]: descending score, equal
+    scores by ascending label, NaN never selected, missing entries -1/-inf.
+    Returns (labels int32 [B,K], scores float64 [B,K])."""
+    z = _f64(z)
+    B, L = z.shape
+    lab = np.empty((B, K), dtype=np.int32)
+    sc = np.empty((B, K), dtype=np.float64)
+    lib().ffslref_topk(B, L, _p(z), K, _p(lab), _p(sc))
+    return lab, sc
+
+
+def precision_at_k(top_lab, off, lab):
+    """P@1..P@K averaged over the samples (float64 [K])."""
+    top_lab = _i32(top_lab)
+    B, K = top_lab.shape
+    off, lab = _i64(off), _i32(lab)
+    out = np.empty(K, dtype=np.float64)
+    lib().ffslref_precision_at_k(B, K, _p(top_lab), _p(off), _p(lab), _p(out))
+    return out
+
+
+def infer_topk(X, W, I, bias, K, off=None, lab=None):
+    """Scores of every label (forward), each sample's top-K, and P@k when the
+    targets are given: the whole inference pass, composed in that order."""
+    z = forward(X, W, I, bias)
+    top, sc = topk(z, K)
+    p = None if off is None else precision_at_k(top, off, lab)
+    return top, sc, p

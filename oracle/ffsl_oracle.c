@@ -525,3 +525,78 @@ EXPORT double ffslref_aux_bce(int64_t B, int64_t d, int64_t C, const double *X,
     free(dZ);
     return loss;
 }
+
+/* ------------------------------------------------------------------------
+ * Inference: the top-k labels of each sample and Precision@k (appendix on
+ * evaluation metrics: P@k of a sample is the fraction of its k best-scored
+ * labels that are relevant).
+ *
+ * Order: descending score, equal scores by ascending label.  Labels whose
+ * score is NaN are never selected; when fewer than K labels can be
+ * selected the remaining entries are label -1 with score -inf.
+ * Plain selection: the j-th entry is the best label that comes after the
+ * (j-1)-th in this order, found by one pass over the row.               */
+EXPORT void ffslref_topk(int64_t B, int64_t L, const double *z, int64_t K,
+                         int32_t *top_lab, double *top_z)
+{
+    for (int64_t b = 0; b < B; ++b) {
+        const double *zr = z + b * L;
+        int64_t prev = -1;
+        double prev_z = 0.0;
+        for (int64_t j = 0; j < K; ++j) {
+            int64_t best = -1;
+            double best_z = 0.0;
+            for (int64_t l = 0; l < L; ++l) {
+                const double v = zr[l];
+                if (v != v)
+                    continue;
+                /* only labels after the previous pick in the order */
+                if (prev >= 0 && !(v < prev_z || (v == prev_z && l > prev)))
+                    continue;
+                if (best < 0 || v > best_z || (v == best_z && l < best)) {
+                    best = l;
+                    best_z = v;
+                }
+            }
+            top_lab[b * K + j] = (int32_t)best;
+            top_z[b * K + j] = best < 0 ? -INFINITY : best_z;
+            if (best < 0) {
+                /* nothing left: the rest of the row stays empty */
+                for (int64_t r = j + 1; r < K; ++r) {
+                    top_lab[b * K + r] = -1;
+                    top_z[b * K + r] = -INFINITY;
+                }
+                break;
+            }
+            prev = best;
+            prev_z = best_z;
+        }
+    }
+}
+
+/* Precision@k for k = 1..K, averaged over the B samples:
+ *     out[k-1] = (1/B) sum_b (1/k) sum_{j<k} y[b, top_lab[b,j]]
+ * y[b,l] = 1 iff l is among the labels lab[off[b] .. off[b+1]) (repeats
+ * count once); an empty entry (label -1) is never relevant.            */
+EXPORT void ffslref_precision_at_k(int64_t B, int64_t K, const int32_t *top_lab,
+                                   const int64_t *off, const int32_t *lab, double *out)
+{
+    for (int64_t k = 0; k < K; ++k)
+        out[k] = 0.0;
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t hits = 0;
+        for (int64_t j = 0; j < K; ++j) {
+            const int32_t t = top_lab[b * K + j];
+            int rel = 0;
+            for (int64_t e = off[b]; e < off[b + 1] && t >= 0; ++e)
+                if (lab[e] == t) {
+                    rel = 1;
+                    break;
+                }
+            hits += rel;
+            out[j] += (double)hits / (double)(j + 1);
+        }
+    }
+    for (int64_t k = 0; k < K; ++k)
+        out[k] /= (double)B;
+}
