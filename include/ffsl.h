@@ -70,6 +70,7 @@ typedef enum {
 #define FFSL_MAX_K 128         /* fan-in                                    */
 #define FFSL_MAX_D 16384       /* input width                               */
 #define FFSL_MAX_B 1024        /* batch size                                */
+#define FFSL_MAX_TOPK 16       /* labels per sample returned by inference   */
 
 typedef struct ffsl_layer ffsl_layer;
 
@@ -205,6 +206,39 @@ FFSL_API int ffsl_train_step_set(ffsl_layer *layer, const void *X, int32_t B,
 FFSL_API int ffsl_set_update(ffsl_layer *layer, float frac, uint64_t seed,
                     uint64_t set_round, uint8_t *pruned_mask_out,
                     int32_t *exhausted_out, void *stream);
+
+/* Bytes of device workspace ffsl_infer_topk needs on this layer for batches of
+ * up to B_max samples and topk labels per sample; 0 if the call would be
+ * rejected (topk outside [1, min(FFSL_MAX_TOPK, L)], B_max outside
+ * [1, FFSL_MAX_B], L >= 2^31, or an X tile of 16 samples and d+1 columns
+ * above the kernel's 144 KiB of LDS: d > 4607 for bf16, d > 2303 for fp32). */
+FFSL_API size_t ffsl_topk_workspace_bytes(const ffsl_layer *layer, int32_t B_max, int32_t topk);
+
+/* Inference: the scores of every label for a batch (the gathered forward of
+ * Sec. 2.2, z[b,l] = bias[l] + sum_j W[l,j] X[b,I[l,j]], fp32 accumulation)
+ * and each sample's topk best labels, with Precision@k (appendix on
+ * evaluation metrics: P@k of a sample is the fraction of its k best-scored
+ * labels that are relevant).  The scores are never written to memory.
+ *   X            [B,d] value_dtype, 1 <= B <= FFSL_MAX_B
+ *   top_labels   int32 [B,topk]: labels by descending score, equal scores by
+ *                ascending label; labels with a NaN score are never chosen,
+ *                and if fewer than topk labels can be chosen the rest of the
+ *                row is -1
+ *   top_scores   nullable fp32 [B,topk]: their scores (-inf where the label
+ *                is -1)
+ *   p_at_k       nullable fp32 [topk]: p_at_k[j] = mean over the B samples
+ *                of P@(j+1); needs tgt_off [B+1] and tgt_lab [nnz] (the
+ *                relevant labels, as in ffsl_forward_loss; repeats count
+ *                once, labels outside [0,L) are never matched)
+ *   workspace    at least ffsl_topk_workspace_bytes(layer, B, topk) bytes,
+ *                256-byte aligned; calls that share it must be ordered
+ * Uses the layer's W, I and bias; writes nothing of the layer.
+ * Errors: FFSL_EINVAL for null required pointers, bad sizes or a short
+ * workspace; FFSL_EUNSUPPORTED for the shapes listed above. */
+FFSL_API int ffsl_infer_topk(ffsl_layer *layer, const void *X, int32_t B, int32_t topk,
+                    int32_t *top_labels, float *top_scores, const int32_t *tgt_off,
+                    const int32_t *tgt_lab, int32_t nnz, float *p_at_k, void *workspace,
+                    size_t workspace_bytes, void *stream);
 
 /* Measurement hook: while both events are non-null, every sweep call
  * (ffsl_forward_loss, ffsl_backward, ffsl_train_step) records `start`

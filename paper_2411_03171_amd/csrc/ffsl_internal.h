@@ -127,6 +127,29 @@ int launch_validate(const Layer &ly, int32_t *bad_rows, hipStream_t st);
 int launch_adam_flat(void *p, int vt, const float *g, float *m, float *v, int64_t n, const AdamParams &ap,
                      int num_cu, hipStream_t st);
 
+// ---------------------------------------------------------------- inference
+
+constexpr size_t TOPK_XS_MAX = 144 * 1024;   // LDS bytes of the staged X tile
+constexpr int TOPK_MAX_WG_PER_CU = 4;         // scan workgroups per CU at most
+
+struct TopkPlan {
+    int spl;      // samples per lane (1, 2, 4)
+    int kp;       // entries per lane list (1, 4, 8, 16)
+    int bt;       // samples per batch tile (16 * spl)
+    int tiles;    // batch tiles
+    int nwg;      // scan workgroups per tile (set by topk_grid)
+    size_t lds;   // dynamic LDS bytes of the scan kernel
+    const void *scan;
+    size_t part, rel, total;   // workspace offsets and size
+};
+// shape of a top-k call (no HIP calls); false if the shape is unsupported
+bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p);
+// grid of the scan kernel on the current device
+int topk_grid(const Layer &ly, TopkPlan *p);
+int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_lab, float *top_sc,
+                const int32_t *off, const int32_t *lab, float *p_at_k, char *ws, const TopkPlan &p,
+                hipStream_t st);
+
 // ---------------------------------------------------------------- dense parts
 
 // workspace of the intermediate layer's backward (byte offsets, 256-aligned)

@@ -1,0 +1,561 @@
+// Inference over the label space: the scores of a batch against every label
+// row (the gathered forward of Sec. 2.2) and, per sample, the labels with the
+// highest scores -- the prediction that Precision@k scores (appendix on
+// evaluation metrics).  The scores never reach memory.
+//
+// k_topk_scan   One persistent workgroup per CU slot and batch tile.  The X
+//               tile is staged in LDS as [d+1][BT] (column d is zero).  A
+//               wave serves 4 label rows at a time, one per DPP row of 16
+//               lanes; a lane serves SPL consecutive samples of the tile.  In
+//               each round of 32 slots, lane u loads slots 2u and 2u+1 of its
+//               row, and row_newbcast hands every slot pair to all 16 lanes of
+//               the row, which gather their samples' X values from LDS.  Each
+//               lane keeps, per sample, the KP best (score, label) keys it
+//               has seen, sorted, in registers; a new key is inserted only
+//               when it beats the last one (one wave-wide test per sample).
+//               At the end the workgroup merges its 32 lists per sample into
+//               one and writes it out.
+// k_topk_merge  One workgroup per sample merges the lists of all
+//               workgroups: K rounds of a block-wide maximum over the heads
+//               of the sorted lists.  Writes labels, scores and relevance.
+// k_patk        Precision@k averaged over the batch.
+//
+// Order of the result: descending score, equal scores by ascending label;
+// NaN scores are never selected.  A (score, label) pair is one 64-bit key
+// that orders exactly that way, so lists compare with one integer compare.
+
+#include "ffsl_internal.h"
+#include "sweep_dev.h"
+
+namespace ffsl {
+namespace {
+using namespace fdev;
+
+constexpr int TK_THREADS = 512;
+constexpr int TK_WAVES = TK_THREADS / 64;
+constexpr int TK_ROWS = 4;                     // label rows per wave per step
+constexpr int TK_LISTS = TK_WAVES * TK_ROWS;   // lists per sample in a workgroup
+constexpr int TK_MERGE_THREADS = 256;
+constexpr int DPP_ROW_NEWBCAST = 0x150;        // + n: lane n of each DPP row to the whole row
+
+struct TkArgs {
+    const void *X;
+    const void *W;
+    const int32_t *I;
+    const float *bias;
+    int64_t L;
+    int32_t B, d, k;
+    int32_t nwg;       // workgroups per batch tile (gridDim.x)
+    uint64_t *part;    // [B][nwg][KP] keys, sorted descending per list
+};
+
+// (score, label) as an integer ordered like (score descending, label
+// ascending): the score's bits mapped to an order-preserving unsigned value
+// (with -0 taken as +0) in the high word, the complemented label in the low
+// word.  Key 0 marks an empty entry; no scored label maps to it.
+__device__ __forceinline__ uint64_t score_key(float z, uint32_t l) {
+    uint32_t u = __float_as_uint(z);
+    u = u == 0x80000000u ? 0u : u;
+    u ^= (u & 0x80000000u) ? 0xffffffffu : 0x80000000u;
+    return ((uint64_t)u << 32) | (uint64_t)(~l);
+}
+
+__device__ __forceinline__ float key_score(uint64_t key) {
+    const uint32_t u = (uint32_t)(key >> 32);
+    return __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
+}
+
+__device__ __forceinline__ int32_t key_label(uint64_t key) { return key ? (int32_t)(~(uint32_t)key) : -1; }
+
+// Insert nk into the descending list kl, dropping the last entry; nk must
+// beat kl[KP-1].
+template <int KP>
+__device__ __forceinline__ void list_insert(uint64_t (&kl)[KP], uint64_t nk) {
+    bool lt[KP];
+#pragma unroll
+    for (int p = 0; p < KP; ++p) lt[p] = kl[p] < nk;
+#pragma unroll
+    for (int p = KP - 1; p > 0; --p) kl[p] = lt[p - 1] ? kl[p - 1] : (lt[p] ? nk : kl[p]);
+    kl[0] = lt[0] ? nk : kl[0];
+}
+
+// Merge the sorted list src[0..KP) (in memory) into kl: entries are taken in
+// order until one does not beat kl's last.
+template <int KP, typename P>
+__device__ __forceinline__ void list_merge(uint64_t (&kl)[KP], const P *src) {
+    for (int p = 0; p < KP; ++p) {
+        const uint64_t key = src[p];
+        if (key <= kl[KP - 1]) break;
+        list_insert(kl, key);
+    }
+}
+
+template <int VT>
+struct TkVal;
+template <>
+struct TkVal<FFSL_BF16> {
+    using T = uint16_t;
+    using Wp = uint32_t;   // the two weights of a slot pair, packed
+};
+template <>
+struct TkVal<FFSL_F32> {
+    using T = float;
+    using Wp = float2;
+};
+
+// row data of one round for this lane as loaded: the columns of its two
+// slots (d for a slot past k: column d of the tile is zero), the two weights
+// and, in round 0, the row's bias.  Converted to LDS offsets only where used,
+// so the loads of the next step stay in flight.
+template <int VT>
+struct TkRaw {
+    int2 c;
+    typename TkVal<VT>::Wp w;
+    float bias;
+};
+
+template <int VT>
+__device__ __forceinline__ void tk_load(const TkArgs &a, int64_t l0, int r, int g, int u, TkRaw<VT> &out) {
+    using T = typename TkVal<VT>::T;
+    const int64_t l = min(l0 + g, a.L - 1);
+    const int s0 = 32 * r + 2 * u;
+    const int64_t base = l * a.k;
+    const T *W = static_cast<const T *>(a.W);
+    if ((a.k & 1) == 0) {
+        // even fan-in: the pair is one aligned load of indices and of weights
+        if (s0 < a.k) {
+            out.c = *reinterpret_cast<const int2 *>(a.I + base + s0);
+            out.w = *reinterpret_cast<const typename TkVal<VT>::Wp *>(W + base + s0);
+        } else {
+            out.c = make_int2(a.d, a.d);
+            if constexpr (VT == FFSL_BF16)
+                out.w = 0u;
+            else
+                out.w = make_float2(0.f, 0.f);
+        }
+    } else {
+        out.c.x = s0 < a.k ? a.I[base + s0] : a.d;
+        out.c.y = s0 + 1 < a.k ? a.I[base + s0 + 1] : a.d;
+        if constexpr (VT == FFSL_BF16) {
+            const uint32_t w0 = s0 < a.k ? W[base + s0] : 0u;
+            const uint32_t w1 = s0 + 1 < a.k ? W[base + s0 + 1] : 0u;
+            out.w = w0 | (w1 << 16);
+        } else {
+            out.w = make_float2(s0 < a.k ? W[base + s0] : 0.f, s0 + 1 < a.k ? W[base + s0 + 1] : 0.f);
+        }
+    }
+    out.bias = (r == 0 && a.bias) ? a.bias[l] : 0.f;
+}
+
+// LDS offsets and weights of a round, ready for the broadcasts
+template <int VT>
+struct TkRound {
+    int32_t o0, o1;
+    typename TkVal<VT>::Wp w;
+};
+
+template <int VT, int SPL>
+__device__ __forceinline__ TkRound<VT> tk_prep(const TkRaw<VT> &raw, int d) {
+    constexpr int COL = 16 * SPL * (int)sizeof(typename TkVal<VT>::T);   // bytes per LDS column
+    // indices outside [0,d) are clamped (the layer's precondition excludes
+    // them); d itself is the zero column
+    const uint32_t c0 = min((uint32_t)raw.c.x, (uint32_t)d), c1 = min((uint32_t)raw.c.y, (uint32_t)d);
+    TkRound<VT> t;
+    t.o0 = (int32_t)c0 * COL;
+    t.o1 = (int32_t)c1 * COL;
+    t.w = raw.w;
+    return t;
+}
+
+template <int CTRL>
+__device__ __forceinline__ int32_t bcast(int32_t x) {
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, true);
+}
+
+template <int VT, int SPL>
+struct TkGather;
+template <> struct TkGather<FFSL_BF16, 4> { using G = uint2; };
+template <> struct TkGather<FFSL_BF16, 2> { using G = uint32_t; };
+template <> struct TkGather<FFSL_BF16, 1> { using G = uint16_t; };
+template <> struct TkGather<FFSL_F32, 4> { using G = float4; };
+template <> struct TkGather<FFSL_F32, 2> { using G = float2; };
+template <> struct TkGather<FFSL_F32, 1> { using G = float; };
+
+// z[e] += w0 * xa[e] + w1 * xb[e] for the lane's samples
+template <int VT, int SPL>
+__device__ __forceinline__ void tk_fma(typename TkGather<VT, SPL>::G xa, typename TkGather<VT, SPL>::G xb,
+                                       typename TkVal<VT>::Wp w, float (&z)[SPL]) {
+    if constexpr (VT == FFSL_BF16) {
+        if constexpr (SPL == 4) {
+            z[0] = dot2(__builtin_amdgcn_perm(xb.x, xa.x, 0x05040100u), w, z[0]);
+            z[1] = dot2(__builtin_amdgcn_perm(xb.x, xa.x, 0x07060302u), w, z[1]);
+            z[2] = dot2(__builtin_amdgcn_perm(xb.y, xa.y, 0x05040100u), w, z[2]);
+            z[3] = dot2(__builtin_amdgcn_perm(xb.y, xa.y, 0x07060302u), w, z[3]);
+        } else if constexpr (SPL == 2) {
+            z[0] = dot2(__builtin_amdgcn_perm(xb, xa, 0x05040100u), w, z[0]);
+            z[1] = dot2(__builtin_amdgcn_perm(xb, xa, 0x07060302u), w, z[1]);
+        } else {
+            z[0] = dot2((uint32_t)xa | ((uint32_t)xb << 16), w, z[0]);
+        }
+    } else {
+        const float *pa = reinterpret_cast<const float *>(&xa);
+        const float *pb = reinterpret_cast<const float *>(&xb);
+#pragma unroll
+        for (int e = 0; e < SPL; ++e) z[e] = fmaf(w.y, pb[e], fmaf(w.x, pa[e], z[e]));
+    }
+}
+
+template <int VT, int N>
+__device__ __forceinline__ typename TkVal<VT>::Wp bcast_w(typename TkVal<VT>::Wp w) {
+    if constexpr (VT == FFSL_BF16)
+        return (uint32_t)bcast<DPP_ROW_NEWBCAST + N>((int32_t)w);
+    else
+        return make_float2(__int_as_float(bcast<DPP_ROW_NEWBCAST + N>(__float_as_int(w.x))),
+                           __int_as_float(bcast<DPP_ROW_NEWBCAST + N>(__float_as_int(w.y))));
+}
+
+// slot pair N of the round (loaded by lane N of the row): gather this lane's
+// samples of the two columns and accumulate
+template <int VT, int SPL, int N>
+__device__ __forceinline__ void tk_pair(const TkRound<VT> &c, int xl, float (&z)[SPL]) {
+    using G = typename TkGather<VT, SPL>::G;
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    const G xa = *reinterpret_cast<const G *>(tk_smem + (xl + bcast<DPP_ROW_NEWBCAST + N>(c.o0)));
+    const G xb = *reinterpret_cast<const G *>(tk_smem + (xl + bcast<DPP_ROW_NEWBCAST + N>(c.o1)));
+    tk_fma<VT, SPL>(xa, xb, bcast_w<VT, N>(c.w), z);
+}
+
+// the round's slot pairs N .. npairs-1 of a partial round (npairs is uniform)
+template <int VT, int SPL, int N = 0>
+__device__ __forceinline__ void tk_round_part(const TkRound<VT> &c, int xl, int npairs,
+                                              float (&z)[SPL]) {
+    if constexpr (N < 16) {
+        if (N < npairs) {
+            tk_pair<VT, SPL, N>(c, xl, z);
+            tk_round_part<VT, SPL, N + 1>(c, xl, npairs, z);
+        }
+    }
+}
+
+// all 16 slot pairs: every gather is issued first, so that they are all in
+// flight together, then the products
+template <int VT, int SPL, int N = 0>
+__device__ __forceinline__ void tk_gather_all(const TkRound<VT> &c, int xl, typename TkGather<VT, SPL>::G (&xa)[16],
+                                              typename TkGather<VT, SPL>::G (&xb)[16]) {
+    if constexpr (N < 16) {
+        using G = typename TkGather<VT, SPL>::G;
+        extern __shared__ __align__(16) unsigned char tk_smem[];
+        xa[N] = *reinterpret_cast<const G *>(tk_smem + (xl + bcast<DPP_ROW_NEWBCAST + N>(c.o0)));
+        xb[N] = *reinterpret_cast<const G *>(tk_smem + (xl + bcast<DPP_ROW_NEWBCAST + N>(c.o1)));
+        tk_gather_all<VT, SPL, N + 1>(c, xl, xa, xb);
+    }
+}
+
+template <int VT, int SPL, int N = 0>
+__device__ __forceinline__ void tk_fma_all(const TkRound<VT> &c, const typename TkGather<VT, SPL>::G (&xa)[16],
+                                           const typename TkGather<VT, SPL>::G (&xb)[16], float (&z)[SPL]) {
+    if constexpr (N < 16) {
+        tk_fma<VT, SPL>(xa[N], xb[N], bcast_w<VT, N>(c.w), z);
+        tk_fma_all<VT, SPL, N + 1>(c, xa, xb, z);
+    }
+}
+
+template <int VT, int SPL>
+__device__ __forceinline__ void tk_round_full(const TkRound<VT> &c, int xl, float (&z)[SPL]) {
+    typename TkGather<VT, SPL>::G xa[16], xb[16];
+    tk_gather_all<VT, SPL>(c, xl, xa, xb);
+    tk_fma_all<VT, SPL>(c, xa, xb, z);
+}
+
+template <int VT, int SPL, int KP>
+__global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
+    using T = typename TkVal<VT>::T;
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    constexpr int BT = 16 * SPL;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, u = lane & 15;
+    const int d = a.d;
+    const int b0 = blockIdx.y * BT;
+    const int nb = min(BT, a.B - b0);
+
+    // stage the tile transposed, Xs[c*BT + b], with a zero column d and zero
+    // samples past B
+    {
+        T *Xs = reinterpret_cast<T *>(tk_smem);
+        const T *X = static_cast<const T *>(a.X) + (int64_t)b0 * d;
+        for (int b = 0; b < BT; ++b)
+            for (int c = tid; c <= d; c += TK_THREADS)
+                Xs[c * BT + b] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
+    }
+    __syncthreads();
+
+    const int xl = u * SPL * (int)sizeof(T);   // LDS byte offset of this lane's samples of column 0
+    // per sample: the sorted list, the score of its last entry once it is
+    // full, and whether it is full
+    uint64_t kl[SPL][KP];
+    float thr[SPL];
+    bool full[SPL];
+#pragma unroll
+    for (int e = 0; e < SPL; ++e) {
+#pragma unroll
+        for (int p = 0; p < KP; ++p) kl[e][p] = 0;
+        thr[e] = -INFINITY;
+        full[e] = false;
+    }
+
+    const int rounds = (a.k + 31) >> 5;
+    const int64_t stride = (int64_t)gridDim.x * TK_WAVES * TK_ROWS;
+    int64_t l0 = ((int64_t)blockIdx.x * TK_WAVES + wave) * TK_ROWS;
+    int r = 0;
+    TkRaw<VT> cur;
+    if (l0 < a.L) tk_load<VT>(a, l0, 0, g, u, cur);
+    float z[SPL];
+#pragma unroll
+    for (int e = 0; e < SPL; ++e) z[e] = 0.f;
+    float zb = 0.f;
+    while (l0 < a.L) {
+        // the next (row group, round) step's row data, loaded ahead
+        int64_t nl0 = l0;
+        int nr = r + 1;
+        if (nr == rounds) {
+            nr = 0;
+            nl0 += stride;
+        }
+        TkRaw<VT> nxt = cur;
+        if (nl0 < a.L) tk_load<VT>(a, nl0, nr, g, u, nxt);
+
+        if (r == 0) zb = cur.bias;
+        const TkRound<VT> rd = tk_prep<VT, SPL>(cur, d);
+        const int npairs = min(16, (a.k - 32 * r + 1) >> 1);
+        if (npairs == 16)
+            tk_round_full<VT, SPL>(rd, xl, z);
+        else
+            tk_round_part<VT, SPL>(rd, xl, npairs, z);
+
+        if (r == rounds - 1) {
+            const int64_t l = l0 + g;
+            const bool valid = l < a.L;
+#pragma unroll
+            for (int e = 0; e < SPL; ++e) {
+                const float ze = z[e] + zb;
+                // this lane's rows come in ascending label order, so a score
+                // equal to the last entry's loses the tie; NaN never enters
+                const bool hit = valid & (u * SPL + e < nb) & ((ze > thr[e]) | (!full[e] & (ze == ze)));
+                if (__builtin_amdgcn_ballot_w64(hit) != 0) {
+                    if (hit) {
+                        list_insert(kl[e], score_key(ze, (uint32_t)l));
+                        full[e] = kl[e][KP - 1] != 0;
+                        thr[e] = full[e] ? key_score(kl[e][KP - 1]) : -INFINITY;
+                    }
+                }
+                z[e] = 0.f;
+            }
+        }
+        cur = nxt;
+        l0 = nl0;
+        r = nr;
+    }
+
+    // merge the workgroup's 32 lists per sample into one
+    __syncthreads();   // the X tile is no longer read
+    uint64_t *Ls = reinterpret_cast<uint64_t *>(tk_smem);
+#pragma unroll
+    for (int e = 0; e < SPL; ++e) {
+        const int bt = u * SPL + e;
+        uint64_t *dst = Ls + ((size_t)bt * TK_LISTS + wave * TK_ROWS + g) * KP;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) dst[p] = kl[e][p];
+    }
+    __syncthreads();
+    constexpr int TPS = TK_THREADS / BT;    // threads per sample
+    constexpr int LPT = TK_LISTS / TPS;     // lists per thread in the first stage
+    const int bt = tid / TPS, sub = tid % TPS;
+    uint64_t m[KP];
+#pragma unroll
+    for (int p = 0; p < KP; ++p) m[p] = 0;
+    if constexpr (LPT > 0) {
+        for (int i = 0; i < LPT; ++i) list_merge(m, Ls + ((size_t)bt * TK_LISTS + sub * LPT + i) * KP);
+    }
+    __syncthreads();
+    uint64_t *Ms = Ls;   // [BT][TPS][KP]
+#pragma unroll
+    for (int p = 0; p < KP; ++p) Ms[((size_t)bt * TPS + sub) * KP + p] = m[p];
+    __syncthreads();
+    if (sub == 0 && bt < nb) {
+        for (int i = 1; i < TPS; ++i) list_merge(m, Ms + ((size_t)bt * TPS + i) * KP);
+        uint64_t *dst = a.part + ((size_t)(b0 + bt) * a.nwg + blockIdx.x) * KP;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) dst[p] = m[p];
+    }
+}
+
+// block-wide maximum of one key per thread (TK_MERGE_THREADS threads)
+__device__ __forceinline__ uint64_t block_max_key(uint64_t x, uint64_t *red) {
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)x, s, 64);
+        const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), s, 64);
+        const uint64_t y = ((uint64_t)hi << 32) | lo;
+        x = y > x ? y : x;
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) red[wave] = x;
+    __syncthreads();
+    uint64_t mx = red[0];
+#pragma unroll
+    for (int w = 1; w < TK_MERGE_THREADS / 64; ++w) mx = red[w] > mx ? red[w] : mx;
+    __syncthreads();
+    return mx;
+}
+
+template <int KP>
+__global__ __launch_bounds__(TK_MERGE_THREADS) void k_topk_merge(const uint64_t *part, int nwg, int K,
+                                                                  int32_t *top_lab, float *top_sc,
+                                                                  const int32_t *off, const int32_t *lab,
+                                                                  uint8_t *rel) {
+    __shared__ uint64_t red[TK_MERGE_THREADS / 64];
+    __shared__ uint64_t win[16];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const uint64_t *pb = part + (size_t)b * nwg * KP;
+    uint64_t kl[KP];
+#pragma unroll
+    for (int p = 0; p < KP; ++p) kl[p] = 0;
+    if (tid < nwg) {
+#pragma unroll
+        for (int p = 0; p < KP; ++p) kl[p] = pb[(size_t)tid * KP + p];
+    }
+    for (int i = tid + TK_MERGE_THREADS; i < nwg; i += TK_MERGE_THREADS) list_merge(kl, pb + (size_t)i * KP);
+    // K rounds: the best head wins and its list moves up by one
+    for (int j = 0; j < K; ++j) {
+        const uint64_t w = block_max_key(kl[0], red);
+        if (w != 0 && kl[0] == w) {
+#pragma unroll
+            for (int p = 0; p < KP - 1; ++p) kl[p] = kl[p + 1];
+            kl[KP - 1] = 0;
+        }
+        if (tid == 0) win[j] = w;
+    }
+    __syncthreads();
+    if (tid < K) {
+        const uint64_t w = win[tid];
+        const int32_t l = key_label(w);
+        top_lab[(size_t)b * K + tid] = l;
+        if (top_sc) top_sc[(size_t)b * K + tid] = w ? key_score(w) : -INFINITY;
+        if (rel) {
+            uint8_t hit = 0;
+            if (l >= 0)
+                for (int e = off[b]; e < off[b + 1]; ++e)
+                    if (lab[e] == l) {
+                        hit = 1;
+                        break;
+                    }
+            rel[(size_t)b * K + tid] = hit;
+        }
+    }
+}
+
+// out[j] = mean over samples of (1/(j+1)) * (relevant among the first j+1)
+__global__ __launch_bounds__(64) void k_patk(const uint8_t *rel, int B, int K, float *out) {
+    const int j = threadIdx.x;
+    if (j >= K) return;
+    int64_t hits = 0;
+    for (int b = 0; b < B; ++b)
+        for (int i = 0; i <= j; ++i) hits += rel[(size_t)b * K + i];
+    out[j] = (float)((double)hits / ((double)(j + 1) * (double)B));
+}
+
+template <int VT, int SPL, int KP>
+const void *scan_kernel() {
+    if constexpr (SPL * KP <= 32)
+        return reinterpret_cast<const void *>(&k_topk_scan<VT, SPL, KP>);
+    else
+        return nullptr;
+}
+
+template <int VT, int SPL>
+const void *pick_kp(int kp) {
+    return kp == 1 ? scan_kernel<VT, SPL, 1>() : kp == 4 ? scan_kernel<VT, SPL, 4>()
+         : kp == 8 ? scan_kernel<VT, SPL, 8>() : scan_kernel<VT, SPL, 16>();
+}
+
+template <int VT>
+const void *pick_spl(int spl, int kp) {
+    return spl == 4 ? pick_kp<VT, 4>(kp) : spl == 2 ? pick_kp<VT, 2>(kp) : pick_kp<VT, 1>(kp);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p) {
+    if (topk < 1 || topk > FFSL_MAX_TOPK || B < 1 || B > FFSL_MAX_B) return false;
+    if (ly.L >= ((int64_t)1 << 31)) return false;
+    const int elt = ly.vt == FFSL_BF16 ? 2 : 4;
+    p->kp = topk == 1 ? 1 : topk <= 4 ? 4 : topk <= 8 ? 8 : 16;
+    int spl = 4;
+    while (spl > 1 &&
+           ((size_t)(ly.d + 1) * 16 * spl * elt > TOPK_XS_MAX || spl * p->kp > 32 || 16 * (spl / 2) >= B))
+        spl /= 2;
+    if ((size_t)(ly.d + 1) * 16 * spl * elt > TOPK_XS_MAX) return false;
+    p->spl = spl;
+    p->bt = 16 * spl;
+    p->tiles = (B + p->bt - 1) / p->bt;
+    p->lds = std::max((size_t)(ly.d + 1) * p->bt * elt, (size_t)TK_THREADS * spl * p->kp * 8);
+    p->scan = ly.vt == FFSL_BF16 ? pick_spl<FFSL_BF16>(spl, p->kp) : pick_spl<FFSL_F32>(spl, p->kp);
+    if (!p->scan) return false;
+    p->nwg = 0;
+    p->part = 0;
+    p->rel = align256(sizeof(uint64_t) * (size_t)B * (size_t)ly.num_cu * TOPK_MAX_WG_PER_CU * p->kp);
+    p->total = p->rel + align256((size_t)B * topk);
+    return true;
+}
+
+int topk_grid(const Layer &ly, TopkPlan *p) {
+    hipError_t e = hipFuncSetAttribute(p->scan, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p->lds);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    int occ = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, p->scan, TK_THREADS, p->lds);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipOccupancyMaxActiveBlocksPerMultiprocessor: %s",
+                                     hipGetErrorString(e));
+    occ = std::max(1, std::min(occ, TOPK_MAX_WG_PER_CU));
+    const int64_t need = (ly.L + TK_LISTS - 1) / TK_LISTS;
+    p->nwg = (int)std::max<int64_t>(1, std::min<int64_t>((int64_t)ly.num_cu * occ, need));
+    return FFSL_OK;
+}
+
+int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_lab, float *top_sc,
+                const int32_t *off, const int32_t *lab, float *p_at_k, char *ws, const TopkPlan &p,
+                hipStream_t st) {
+    TkArgs a{};
+    a.X = X;
+    a.W = ly.W;
+    a.I = ly.I;
+    a.bias = ly.bias;
+    a.L = ly.L;
+    a.B = B;
+    a.d = ly.d;
+    a.k = ly.k;
+    a.nwg = p.nwg;
+    a.part = reinterpret_cast<uint64_t *>(ws + p.part);
+    uint8_t *rel = p_at_k ? reinterpret_cast<uint8_t *>(ws + p.rel) : nullptr;
+    hipLaunchKernelGGL(reinterpret_cast<void (*)(TkArgs)>(const_cast<void *>(p.scan)), dim3(p.nwg, p.tiles),
+                       dim3(TK_THREADS), p.lds, st, a);
+    int rc = check_launch("k_topk_scan");
+    if (rc) return rc;
+    switch (p.kp) {
+    case 1: hipLaunchKernelGGL(k_topk_merge<1>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                               top_lab, top_sc, off, lab, rel); break;
+    case 4: hipLaunchKernelGGL(k_topk_merge<4>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                               top_lab, top_sc, off, lab, rel); break;
+    case 8: hipLaunchKernelGGL(k_topk_merge<8>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                               top_lab, top_sc, off, lab, rel); break;
+    default: hipLaunchKernelGGL(k_topk_merge<16>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                                top_lab, top_sc, off, lab, rel); break;
+    }
+    rc = check_launch("k_topk_merge");
+    if (rc || !p_at_k) return rc;
+    hipLaunchKernelGGL(k_patk, dim3(1), dim3(64), 0, st, rel, B, topk, p_at_k);
+    return check_launch("k_patk");
+}
+
+}  // namespace ffsl

@@ -37,6 +37,8 @@ SIGNATURES = {
                                    _f32, _vp, _vp, _u32, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_set_update": (_int, [_vp, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_validate_indices": (_int, [_vp, _vp, _vp]),
+    "ffsl_topk_workspace_bytes": (_sz, [_vp, _i32, _i32]),
+    "ffsl_infer_topk": (_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "ffsl_set_timing_events": (_int, [_vp, _vp, _vp]),
     "ffsl_dense_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "ffsl_dense_gelu_fwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
@@ -260,6 +262,37 @@ class SparseLayer:
     def set_timing_events(self, start, stop):
         """Raw hipEvent_t handles (ints) or None; see ffsl_set_timing_events."""
         _check(load().ffsl_set_timing_events(self._handle, start, stop))
+
+    def infer_topk(self, X, topk, off=None, lab=None, scores=True, workspace=None):
+        """Each sample's topk labels (int32 [B, topk]), their scores (fp32, or
+        None) and, when the relevant labels are given, P@1..P@topk averaged
+        over the batch (fp32 [topk], or None)."""
+        torch = self.torch
+        if X.dim() != 2 or X.shape[1] != self.d:
+            raise ValueError("X must be [B, %d]" % self.d)
+        want = torch.bfloat16 if self.vt == FFSL_BF16 else torch.float32
+        if X.dtype != want or not X.is_cuda or not X.is_contiguous():
+            raise TypeError("X must be a contiguous %s CUDA tensor" % want)
+        B = X.shape[0]
+        lib = load()
+        need = lib.ffsl_topk_workspace_bytes(self._handle, B, int(topk))
+        if need == 0:
+            raise FfslError(FFSL_EUNSUPPORTED, "top-k inference: unsupported shape or topk")
+        ws = workspace if workspace is not None else _workspace(torch, need, X.device)
+        top = torch.empty((B, topk), dtype=torch.int32, device=X.device)
+        sc = torch.empty((B, topk), dtype=torch.float32, device=X.device) if scores else None
+        p = None
+        nnz = 0
+        if off is not None:
+            off = off.to(device=X.device, dtype=torch.int32).contiguous()
+            lab = lab.to(device=X.device, dtype=torch.int32).contiguous()
+            if off.numel() != B + 1:
+                raise ValueError("tgt_off must have B+1 entries")
+            nnz = int(lab.numel())
+            p = torch.empty(topk, dtype=torch.float32, device=X.device)
+        _check(lib.ffsl_infer_topk(self._handle, _ptr(X), B, int(topk), _ptr(top), _ptr(sc), _ptr(off),
+                                   _ptr(lab), nnz, _ptr(p), _ptr(ws), ws.numel(), _stream(torch)))
+        return top, sc, p
 
     def validate_indices(self):
         torch = self.torch
