@@ -246,6 +246,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--set-reps", type=int, default=10)
     ap.add_argument("--dense-reps", type=int, default=20)
+    ap.add_argument("--infer-reps", type=int, default=10,
+                    help="timed top-k inference calls (0 skips them)")
     ap.add_argument("--hinge-reps", type=int, default=10,
                     help="squared hinge steps per case (0 skips them, e.g. under a kernel trace "
                          "whose per-kernel average should cover the BCE step only)")
@@ -407,6 +409,30 @@ def main():
         print("[bench] squared hinge step: %.3f ms (dense dlogits), %.3f ms (past the margin); BCE %.3f ms" %
               (hinge["dense_dlogits"], hinge["past_margin"], plain_med), file=sys.stderr, flush=True)
 
+    # inference over the whole label space: each sample's top 5 labels and
+    # P@1..P@5 (the scores never reach memory)
+    infer = None
+    if args.infer_reps > 0:
+        K_INF = 5
+        lib = ffsl.load()
+        ws_inf = torch.empty(max(int(lib.ffsl_topk_workspace_bytes(layer._handle, w.B, K_INF)), 256),
+                             dtype=torch.uint8, device=dev)
+        layer.infer_topk(X, K_INF, off, lab, workspace=ws_inf)   # first call sets the kernel up
+        torch.cuda.synchronize()
+        im = sorted(one_step(lambda: layer.infer_topk(X, K_INF, off, lab, workspace=ws_inf))
+                    for _ in range(args.infer_reps))
+        inf_ms = im[len(im) // 2]
+        inf_bytes = w.L * w.k * (vb + 4) + 4 * w.L + w.B * w.d * vb
+        inf_gbs = inf_bytes / (inf_ms * 1e-3) / 1e9
+        # every (label row, slot, sample) reads one X value from LDS
+        lds_bytes = w.L * w.k * w.B * vb
+        infer = {"topk": K_INF, "ms_median": inf_ms, "algorithmic_bytes": inf_bytes, "achieved": inf_gbs,
+                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": inf_gbs / HBM_PEAK_GBS,
+                 "lds_gather_bytes": lds_bytes,
+                 "sample_labels_per_s": w.B * w.L / (inf_ms * 1e-3)}
+        print("[bench] inference top-%d: %.3f ms median, %.0f GB/s algorithmic (%.1f%% of HBM peak)" %
+              (K_INF, inf_ms, inf_gbs, 100 * inf_gbs / HBM_PEAK_GBS), file=sys.stderr, flush=True)
+
     dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
@@ -468,6 +494,7 @@ def main():
             "bce_step_ms_median": plain_med,
             "note": "FFSL_LOSS_SQHINGE; past_margin: bias -4, dW work skipped where a wave has no dlogit",
         },
+        "infer_topk": infer,
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],
         "cpu_baseline": cpu,

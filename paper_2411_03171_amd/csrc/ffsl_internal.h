@@ -139,6 +139,7 @@ struct TopkPlan {
     int tiles;    // batch tiles
     int nwg;      // scan workgroups per tile (set by topk_grid)
     size_t lds;   // dynamic LDS bytes of the scan kernel
+    int thr_off;  // LDS byte offset of the per-sample bounds (after the X tile)
     const void *scan;
     size_t part, rel, total;   // workspace offsets and size
 };

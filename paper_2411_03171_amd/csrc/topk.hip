@@ -36,6 +36,7 @@ constexpr int TK_WAVES = TK_THREADS / 64;
 constexpr int TK_ROWS = 4;                     // label rows per wave per step
 constexpr int TK_LISTS = TK_WAVES * TK_ROWS;   // lists per sample in a workgroup
 constexpr int TK_MERGE_THREADS = 256;
+constexpr int TK_AHEAD = 8;                    // steps of row data loaded ahead
 constexpr int DPP_ROW_NEWBCAST = 0x150;        // + n: lane n of each DPP row to the whole row
 
 struct TkArgs {
@@ -46,6 +47,9 @@ struct TkArgs {
     int64_t L;
     int32_t B, d, k;
     int32_t nwg;       // workgroups per batch tile (gridDim.x)
+    int32_t thr_off;   // LDS byte offset of the per-sample shared bounds, then
+                       // of the best score of each of the 32 lists per sample
+    int32_t K;         // labels wanted per sample
     uint64_t *part;    // [B][nwg][KP] keys, sorted descending per list
 };
 
@@ -60,9 +64,10 @@ __device__ __forceinline__ uint64_t score_key(float z, uint32_t l) {
     return ((uint64_t)u << 32) | (uint64_t)(~l);
 }
 
+// the score of a key (-inf for the empty key 0)
 __device__ __forceinline__ float key_score(uint64_t key) {
     const uint32_t u = (uint32_t)(key >> 32);
-    return __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
+    return u == 0u ? -INFINITY : __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
 }
 
 __device__ __forceinline__ int32_t key_label(uint64_t key) { return key ? (int32_t)(~(uint32_t)key) : -1; }
@@ -286,74 +291,141 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
         for (int b = 0; b < BT; ++b)
             for (int c = tid; c <= d; c += TK_THREADS)
                 Xs[c * BT + b] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
+        for (int i = tid; i < BT * (1 + TK_LISTS); i += TK_THREADS)
+            reinterpret_cast<uint32_t *>(tk_smem + a.thr_off)[i] = 0u;
     }
     __syncthreads();
 
     const int xl = u * SPL * (int)sizeof(T);   // LDS byte offset of this lane's samples of column 0
-    // per sample: the sorted list, the score of its last entry once it is
-    // full, and whether it is full
+    // Per sample: the lane's sorted list, the score of its last entry once it
+    // is full, and whether it is full.  Shared by the workgroup: per sample the
+    // highest last-entry score of any full list (as an order-preserving
+    // integer, 0 = none), a bound below which no label can still make the
+    // sample's top KP; a score equal to it may, by its label, so it passes.
     uint64_t kl[SPL][KP];
-    float thr[SPL];
+    float thr[SPL], thr_sh[SPL];
     bool full[SPL];
 #pragma unroll
     for (int e = 0; e < SPL; ++e) {
 #pragma unroll
         for (int p = 0; p < KP; ++p) kl[e][p] = 0;
         thr[e] = -INFINITY;
+        thr_sh[e] = -INFINITY;
         full[e] = false;
     }
+    uint32_t *shared_thr = reinterpret_cast<uint32_t *>(tk_smem + a.thr_off);
+    // lmax[bt * TK_LISTS + list]: best score of each list (0 = empty).  The
+    // K-th largest of a sample's 32 list bests is also a bound: K distinct
+    // labels reach it.
+    uint32_t *lmax = shared_thr + BT;
+    const int my_list = wave * TK_ROWS + g;
 
     const int rounds = (a.k + 31) >> 5;
     const int64_t stride = (int64_t)gridDim.x * TK_WAVES * TK_ROWS;
     int64_t l0 = ((int64_t)blockIdx.x * TK_WAVES + wave) * TK_ROWS;
     int r = 0;
-    TkRaw<VT> cur;
-    if (l0 < a.L) tk_load<VT>(a, l0, 0, g, u, cur);
+    // ring of row data, TK_AHEAD steps of (row group, round) ahead
+    TkRaw<VT> ring[TK_AHEAD];
+    int64_t ll0 = l0;
+    int lr = 0;
+#pragma unroll
+    for (int i = 0; i < TK_AHEAD; ++i) {
+        if (ll0 < a.L) tk_load<VT>(a, ll0, lr, g, u, ring[i]);
+        if (++lr == rounds) {
+            lr = 0;
+            ll0 += stride;
+        }
+    }
     float z[SPL];
 #pragma unroll
     for (int e = 0; e < SPL; ++e) z[e] = 0.f;
     float zb = 0.f;
-    while (l0 < a.L) {
-        // the next (row group, round) step's row data, loaded ahead
-        int64_t nl0 = l0;
-        int nr = r + 1;
-        if (nr == rounds) {
-            nr = 0;
-            nl0 += stride;
-        }
-        TkRaw<VT> nxt = cur;
-        if (nl0 < a.L) tk_load<VT>(a, nl0, nr, g, u, nxt);
-
-        if (r == 0) zb = cur.bias;
-        const TkRound<VT> rd = tk_prep<VT, SPL>(cur, d);
-        const int npairs = min(16, (a.k - 32 * r + 1) >> 1);
-        if (npairs == 16)
-            tk_round_full<VT, SPL>(rd, xl, z);
-        else
-            tk_round_part<VT, SPL>(rd, xl, npairs, z);
-
-        if (r == rounds - 1) {
-            const int64_t l = l0 + g;
-            const bool valid = l < a.L;
+    bool more = l0 < a.L;
+    int steps = 0;
+    while (more) {
 #pragma unroll
-            for (int e = 0; e < SPL; ++e) {
-                const float ze = z[e] + zb;
-                // this lane's rows come in ascending label order, so a score
-                // equal to the last entry's loses the tie; NaN never enters
-                const bool hit = valid & (u * SPL + e < nb) & ((ze > thr[e]) | (!full[e] & (ze == ze)));
-                if (__builtin_amdgcn_ballot_w64(hit) != 0) {
-                    if (hit) {
-                        list_insert(kl[e], score_key(ze, (uint32_t)l));
-                        full[e] = kl[e][KP - 1] != 0;
-                        thr[e] = full[e] ? key_score(kl[e][KP - 1]) : -INFINITY;
+        for (int i = 0; i < TK_AHEAD; ++i) {
+            if (more) {   // uniform
+                const TkRaw<VT> cur = ring[i];
+                if (ll0 < a.L) tk_load<VT>(a, ll0, lr, g, u, ring[i]);
+                if (++lr == rounds) {
+                    lr = 0;
+                    ll0 += stride;
+                }
+
+                if (r == 0) zb = cur.bias;
+                const TkRound<VT> rd = tk_prep<VT, SPL>(cur, d);
+                const int npairs = min(16, (a.k - 32 * r + 1) >> 1);
+                if (npairs == 16)
+                    tk_round_full<VT, SPL>(rd, xl, z);
+                else
+                    tk_round_part<VT, SPL>(rd, xl, npairs, z);
+
+                if (r == rounds - 1) {
+                    const int64_t l = l0 + g;
+                    const bool valid = l < a.L;
+                    ++steps;
+                    if ((steps & (steps - 1)) == 0 || (steps & 63) == 0) {
+                        // every wave turns the list bests of 8 samples into
+                        // bounds, after 1, 2, 4, ... rows and then every 64
+                        if (lane < BT / TK_WAVES) {
+                            const int bt = wave * (BT / TK_WAVES) + lane;
+                            uint32_t best[KP];
+#pragma unroll
+                            for (int p = 0; p < KP; ++p) best[p] = 0u;
+                            for (int i = 0; i < TK_LISTS; ++i) {
+                                uint32_t v = __hip_atomic_load(lmax + bt * TK_LISTS + i, __ATOMIC_RELAXED,
+                                                               __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+                                for (int p = 0; p < KP; ++p) {
+                                    const uint32_t hi = max(best[p], v), lo = min(best[p], v);
+                                    best[p] = hi;
+                                    v = lo;
+                                }
+                            }
+                            uint32_t vk = 0u;
+#pragma unroll
+                            for (int p = 0; p < KP; ++p) vk = p == a.K - 1 ? best[p] : vk;
+                            atomicMax(shared_thr + bt, vk);
+                        }
+                    }
+                    if ((steps & 3) == 0) {
+                        // refresh the workgroup's bounds for this lane's samples
+#pragma unroll
+                        for (int e = 0; e < SPL; ++e)
+                            thr_sh[e] = key_score((uint64_t)__hip_atomic_load(shared_thr + u * SPL + e, __ATOMIC_RELAXED,
+                                                                              __HIP_MEMORY_SCOPE_WORKGROUP)
+                                                  << 32);
+                    }
+#pragma unroll
+                    for (int e = 0; e < SPL; ++e) {
+                        const float ze = z[e] + zb;
+                        // this lane's rows come in ascending label order, so a
+                        // score equal to its own last entry's loses the tie;
+                        // NaN never enters
+                        const bool hit = valid & (u * SPL + e < nb) & ((ze > thr[e]) | (!full[e] & (ze == ze))) &
+                                         (ze >= thr_sh[e]);
+                        if (__builtin_amdgcn_ballot_w64(hit) != 0) {
+                            if (hit) {
+                                list_insert(kl[e], score_key(ze, (uint32_t)l));
+                                lmax[(u * SPL + e) * TK_LISTS + my_list] = (uint32_t)(kl[e][0] >> 32);
+                                full[e] = kl[e][KP - 1] != 0;
+                                if (full[e]) {
+                                    thr[e] = key_score(kl[e][KP - 1]);
+                                    atomicMax(shared_thr + u * SPL + e, (uint32_t)(kl[e][KP - 1] >> 32));
+                                }
+                            }
+                        }
+                        z[e] = 0.f;
                     }
                 }
-                z[e] = 0.f;
+                if (++r == rounds) {
+                    r = 0;
+                    l0 += stride;
+                }
+                more = l0 < a.L;
             }
         }
-        cur = nxt;
-        l0 = nl0;
-        r = nr;
     }
 
     // merge the workgroup's 32 lists per sample into one
@@ -455,18 +527,36 @@ __global__ __launch_bounds__(TK_MERGE_THREADS) void k_topk_merge(const uint64_t 
 }
 
 // out[j] = mean over samples of (1/(j+1)) * (relevant among the first j+1)
-__global__ __launch_bounds__(64) void k_patk(const uint8_t *rel, int B, int K, float *out) {
-    const int j = threadIdx.x;
-    if (j >= K) return;
-    int64_t hits = 0;
-    for (int b = 0; b < B; ++b)
-        for (int i = 0; i <= j; ++i) hits += rel[(size_t)b * K + i];
-    out[j] = (float)((double)hits / ((double)(j + 1) * (double)B));
+constexpr int TK_PATK_THREADS = 256;
+__global__ __launch_bounds__(TK_PATK_THREADS) void k_patk(const uint8_t *rel, int B, int K, float *out) {
+    __shared__ int32_t part[16][TK_PATK_THREADS];
+    const int t = threadIdx.x;
+    int32_t acc[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] = 0;
+    for (int b = t; b < B; b += TK_PATK_THREADS) {
+        int32_t h = 0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            if (j < K) h += rel[(size_t)b * K + j];
+            acc[j] += h;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) part[j][t] = acc[j];
+    __syncthreads();
+    for (int s = TK_PATK_THREADS / 2; s > 0; s >>= 1) {
+        if (t < s)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) part[j][t] += part[j][t + s];
+        __syncthreads();
+    }
+    if (t < K) out[t] = (float)((double)part[t][0] / ((double)(t + 1) * (double)B));
 }
 
 template <int VT, int SPL, int KP>
 const void *scan_kernel() {
-    if constexpr (SPL * KP <= 32)
+    if constexpr (SPL * KP <= (VT == FFSL_BF16 ? 32 : 16))
         return reinterpret_cast<const void *>(&k_topk_scan<VT, SPL, KP>);
     else
         return nullptr;
@@ -492,15 +582,19 @@ bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p) {
     if (ly.L >= ((int64_t)1 << 31)) return false;
     const int elt = ly.vt == FFSL_BF16 ? 2 : 4;
     p->kp = topk == 1 ? 1 : topk <= 4 ? 4 : topk <= 8 ? 8 : 16;
+    // list registers per lane: spl * kp keys (fp32 lanes also hold wider gathers)
+    const int max_keys = ly.vt == FFSL_BF16 ? 32 : 16;
     int spl = 4;
     while (spl > 1 &&
-           ((size_t)(ly.d + 1) * 16 * spl * elt > TOPK_XS_MAX || spl * p->kp > 32 || 16 * (spl / 2) >= B))
+           ((size_t)(ly.d + 1) * 16 * spl * elt > TOPK_XS_MAX || spl * p->kp > max_keys || 16 * (spl / 2) >= B))
         spl /= 2;
     if ((size_t)(ly.d + 1) * 16 * spl * elt > TOPK_XS_MAX) return false;
     p->spl = spl;
     p->bt = 16 * spl;
     p->tiles = (B + p->bt - 1) / p->bt;
-    p->lds = std::max((size_t)(ly.d + 1) * p->bt * elt, (size_t)TK_THREADS * spl * p->kp * 8);
+    p->thr_off = (int)align256((size_t)(ly.d + 1) * p->bt * elt);
+    p->lds = std::max((size_t)p->thr_off + sizeof(uint32_t) * p->bt * (1 + TK_LISTS),
+                      (size_t)TK_THREADS * spl * p->kp * 8);
     p->scan = ly.vt == FFSL_BF16 ? pick_spl<FFSL_BF16>(spl, p->kp) : pick_spl<FFSL_F32>(spl, p->kp);
     if (!p->scan) return false;
     p->nwg = 0;
@@ -536,6 +630,8 @@ int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_la
     a.d = ly.d;
     a.k = ly.k;
     a.nwg = p.nwg;
+    a.thr_off = p.thr_off;
+    a.K = topk;
     a.part = reinterpret_cast<uint64_t *>(ws + p.part);
     uint8_t *rel = p_at_k ? reinterpret_cast<uint8_t *>(ws + p.rel) : nullptr;
     hipLaunchKernelGGL(reinterpret_cast<void (*)(TkArgs)>(const_cast<void *>(p.scan)), dim3(p.nwg, p.tiles),
@@ -554,7 +650,7 @@ int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_la
     }
     rc = check_launch("k_topk_merge");
     if (rc || !p_at_k) return rc;
-    hipLaunchKernelGGL(k_patk, dim3(1), dim3(64), 0, st, rel, B, topk, p_at_k);
+    hipLaunchKernelGGL(k_patk, dim3(1), dim3(TK_PATK_THREADS), 0, st, rel, B, topk, p_at_k);
     return check_launch("k_patk");
 }
 
