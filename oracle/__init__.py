@@ -62,6 +62,9 @@ def lib():
         L.ffslref_set_update.argtypes = [i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
                                          dbl, u64, u64, ctypes.c_int, u64]
         L.ffslref_set_update.restype = i64
+        L.ffslref_set_update_threshold.argtypes = [i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
+                                                   dbl, u64, u64, ctypes.c_int, u64]
+        L.ffslref_set_update_threshold.restype = i64
         L.ffslref_dense_gelu_fwd.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp]
         L.ffslref_dense_gelu_fwd.restype = None
         L.ffslref_dense_gelu_bwd.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
@@ -245,6 +248,31 @@ def set_update(Wbits, I, m, v, d, frac, seed, set_round, allow_regrow_pruned=Fal
 
 # --------------------------------------------------------------------------
 # dense parts
+
+def set_update_threshold(Wbits, I, m, v, d, tau, seed, set_round, allow_regrow_pruned=False, row0=0):
+    """SET in threshold mode (every slot with |W| < tau is pruned, as many
+    columns regrown in its row) on copies of the state; arguments and result
+    as set_update."""
+    Wb = np.ascontiguousarray(Wbits).copy()
+    if Wb.dtype == np.uint16:
+        wbits = 16
+    elif Wb.dtype == np.uint32:
+        wbits = 32
+    else:
+        raise TypeError("Wbits must be uint16 or uint32 bit patterns")
+    L, k = Wb.shape
+    Ic = _i32(I).copy()
+    mc = None if m is None else np.ascontiguousarray(m, dtype=np.float32).copy()
+    vc = None if v is None else np.ascontiguousarray(v, dtype=np.float32).copy()
+    mask = np.empty((L, k), dtype=np.uint8)
+    ex = lib().ffslref_set_update_threshold(L, int(d), k, wbits, _p(Wb), _p(Ic), _p(mc), _p(vc),
+                                            _p(mask), float(tau), int(seed) & (2**64 - 1),
+                                            int(set_round) & (2**64 - 1), int(bool(allow_regrow_pruned)),
+                                            int(row0))
+    if ex < 0:
+        raise ValueError("invalid SET arguments")
+    return Wb, Ic, mc, vc, mask, int(ex)
+
 
 def dense_gelu_fwd(X, W1, c=None):
     X, W1 = _f64(X), _f64(W1)

@@ -303,51 +303,85 @@ EXPORT int64_t ffslref_set_prune_count(int64_t k, double frac)
     return (int64_t)floor(frac * (double)k + 1e-9);
 }
 
-EXPORT int64_t ffslref_set_update(int64_t L, int64_t d, int64_t k, int wbits,
-                                  void *Wbits, int32_t *I, float *m, float *v,
-                                  uint8_t *mask, double frac, uint64_t seed,
-                                  uint64_t set_round, int allow_regrow_pruned,
-                                  uint64_t row0)
+/* The magnitude of stored weight j of row l as a real number. */
+static double set_magnitude(int wbits, const void *Wbits, int64_t o)
 {
-    int64_t n = ffslref_set_prune_count(k, frac);
-    if (n < 0 || n > k || (wbits != 16 && wbits != 32))
+    if (wbits == 16) {
+        const uint32_t u = (uint32_t)(((const uint16_t *)Wbits)[o] & 0x7fffu) << 16;
+        float f;
+        memcpy(&f, &u, 4);
+        return (double)f;
+    }
+    const uint32_t u = ((const uint32_t *)Wbits)[o] & 0x7fffffffu;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+/* SET over rows, in one of two prune modes (Sec. 2.1; the appendix table of
+ * DST settings lists both):
+ *   fraction   the n = floor(frac*k) smallest keys (|W| bits, slot) of every row
+ *   threshold  the slots of a row with |W| < tau (NaN is never below), so n
+ *              varies by row
+ * then the same regrowth for the n pruned slots of each row. */
+static int64_t set_update_rows(int64_t L, int64_t d, int64_t k, int wbits, void *Wbits,
+                               int32_t *I, float *m, float *v, uint8_t *mask, int threshold,
+                               double frac, double tau, uint64_t seed, uint64_t set_round,
+                               int allow_regrow_pruned, uint64_t row0)
+{
+    const int64_t nf = ffslref_set_prune_count(k, frac);
+    if (wbits != 16 && wbits != 32)
         return -1;
-    if (!allow_regrow_pruned && n > d - k)
+    if (!threshold && (nf < 0 || nf > k || (!allow_regrow_pruned && nf > d - k)))
+        return -1;
+    if (threshold && !(tau >= 0.0))
         return -1;
     if (mask)
         memset(mask, 0, (size_t)(L * k));
-    if (n == 0)
+    if (!threshold && nf == 0)
         return 0;
 
     uint64_t *keys = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)k);
-    int64_t *pruned = (int64_t *)malloc(sizeof(int64_t) * (size_t)n);
-    int32_t *accepted = (int32_t *)malloc(sizeof(int32_t) * (size_t)n);
+    int64_t *pruned = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
+    int32_t *accepted = (int32_t *)malloc(sizeof(int32_t) * (size_t)k);
     uint8_t *taken = (uint8_t *)malloc((size_t)k);
     int64_t exhausted = 0;
     const int64_t cap = 64 * k + 4096;
 
     for (int64_t l = 0; l < L; ++l) {
-        /* keys of the row */
-        for (int64_t j = 0; j < k; ++j) {
-            uint64_t mag;
-            if (wbits == 16)
-                mag = ((uint16_t *)Wbits)[l * k + j] & 0x7fffu;
-            else
-                mag = ((uint32_t *)Wbits)[l * k + j] & 0x7fffffffu;
-            keys[j] = mag;
-        }
-        /* select the n smallest (mag, slot) by repeated minimum search */
         memset(taken, 0, (size_t)k);
-        for (int64_t s = 0; s < n; ++s) {
-            int64_t best = -1;
+        int64_t n = 0;
+        if (threshold) {
+            for (int64_t j = 0; j < k; ++j)
+                if (set_magnitude(wbits, Wbits, l * k + j) < tau) {
+                    taken[j] = 1;
+                    ++n;
+                }
+        } else {
+            /* keys of the row */
             for (int64_t j = 0; j < k; ++j) {
-                if (taken[j])
-                    continue;
-                if (best < 0 || keys[j] < keys[best])
-                    best = j; /* strict <: the smaller slot wins ties */
+                uint64_t mag;
+                if (wbits == 16)
+                    mag = ((uint16_t *)Wbits)[l * k + j] & 0x7fffu;
+                else
+                    mag = ((uint32_t *)Wbits)[l * k + j] & 0x7fffffffu;
+                keys[j] = mag;
             }
-            taken[best] = 1;
+            /* select the n smallest (mag, slot) by repeated minimum search */
+            n = nf;
+            for (int64_t s = 0; s < n; ++s) {
+                int64_t best = -1;
+                for (int64_t j = 0; j < k; ++j) {
+                    if (taken[j])
+                        continue;
+                    if (best < 0 || keys[j] < keys[best])
+                        best = j; /* strict <: the smaller slot wins ties */
+                }
+                taken[best] = 1;
+            }
         }
+        if (n == 0)
+            continue;
         int64_t np = 0;
         for (int64_t j = 0; j < k; ++j)
             if (taken[j])
@@ -400,6 +434,28 @@ EXPORT int64_t ffslref_set_update(int64_t L, int64_t d, int64_t k, int wbits,
     free(accepted);
     free(taken);
     return exhausted;
+}
+
+EXPORT int64_t ffslref_set_update(int64_t L, int64_t d, int64_t k, int wbits,
+                                  void *Wbits, int32_t *I, float *m, float *v,
+                                  uint8_t *mask, double frac, uint64_t seed,
+                                  uint64_t set_round, int allow_regrow_pruned,
+                                  uint64_t row0)
+{
+    return set_update_rows(L, d, k, wbits, Wbits, I, m, v, mask, 0, frac, 0.0, seed, set_round,
+                           allow_regrow_pruned, row0);
+}
+
+/* SET in threshold mode: every slot with |W| < tau is pruned and as many
+ * columns are regrown in its row (the appendix's "rewire threshold"). */
+EXPORT int64_t ffslref_set_update_threshold(int64_t L, int64_t d, int64_t k, int wbits,
+                                            void *Wbits, int32_t *I, float *m, float *v,
+                                            uint8_t *mask, double tau, uint64_t seed,
+                                            uint64_t set_round, int allow_regrow_pruned,
+                                            uint64_t row0)
+{
+    return set_update_rows(L, d, k, wbits, Wbits, I, m, v, mask, 1, 0.0, tau, seed, set_round,
+                           allow_regrow_pruned, row0);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -231,3 +231,98 @@ def test_set_row_block_equals_whole_layer(oracle):
     assert np.array_equal(whole[4][150:260], blk[4])
     _, Ir, _ = python_set(W[150:260], I[150:260], 96, 0.25, 11, 2, row0=150)
     assert np.array_equal(Ir, blk[1])
+
+
+# --------------------------------------------------------------------------
+# threshold prune mode (the appendix's "rewire threshold")
+
+def values_of(Wbits):
+    if Wbits.dtype == np.uint16:
+        return synth.bf16_bits_to_f32(Wbits).astype(np.float64)
+    return Wbits.view(np.float32).astype(np.float64)
+
+
+def python_set_threshold(Wbits, I, d, tau, seed, set_round, row0=0):
+    """Threshold SET re-derived in plain Python: the slots with |W| < tau
+    (decoded to real numbers here) are pruned, regrowth as in python_set."""
+    Wb, I = Wbits.copy(), I.copy()
+    L, k = I.shape
+    mask = np.zeros((L, k), dtype=np.uint8)
+    cap = 64 * k + 4096
+    mags = np.abs(values_of(Wbits))
+    ex = 0
+    for l in range(L):
+        pruned = [j for j in range(k) if mags[l, j] < tau]
+        n = len(pruned)
+        pre = set(I[l].tolist())
+        acc = []
+        block = None
+        for a in range(cap):
+            if len(acc) == n:
+                break
+            if a % 4 == 0:
+                block = numpy_philox_block((row0 + l, set_round, a // 4, 0), (seed, SET_KEY_HI))
+            c = (int(block[a % 4]) * d) >> 64
+            if c not in pre and c not in acc:
+                acc.append(c)
+        if len(acc) < n:
+            ex += 1
+            continue
+        for p, c in zip(pruned, acc):
+            I[l, p] = c
+            Wb[l, p] = 0
+            mask[l, p] = 1
+    return Wb, I, mask, ex
+
+
+@pytest.mark.parametrize("value", ["bf16", "f32"])
+@pytest.mark.parametrize("tau", [0.05, 0.01, 0.125])
+def test_set_threshold_matches_python_contract(oracle, value, tau):
+    L, k, d = 300, 16, 64
+    W, I, m, v = make_state(19, L, k, d, value, ties=(tau == 0.125))
+    if value == "f32":
+        W = W.copy()
+        W[5, 3] = np.float32(np.nan).view(np.uint32)      # NaN is never below tau
+    W1, I1, m1, v1, mask, ex = oracle.set_update_threshold(W, I, m, v, d, tau, seed=77, set_round=2)
+    Wr, Ir, maskr, exr = python_set_threshold(W, I, d, tau, 77, 2)
+    assert ex == exr == 0
+    assert np.array_equal(I1, Ir) and np.array_equal(mask, maskr) and np.array_equal(W1, Wr)
+    # per-row counts equal the number of magnitudes below tau; the rest of the contract
+    n_row = (np.abs(values_of(W)) < tau).sum(axis=1)
+    assert np.array_equal(mask.sum(axis=1), n_row)
+    assert n_row.min() < n_row.max()                        # the count really varies by row
+    for l in range(L):
+        assert len(set(I1[l].tolist())) == k
+        assert not (set(I1[l][mask[l] == 1].tolist()) & set(I[l].tolist()))
+    keep = mask == 0
+    assert np.array_equal(W1[keep], W[keep]) and np.array_equal(m1[keep], m[keep])
+    assert np.all(W1[~keep] == 0) and np.all(m1[~keep] == 0) and np.all(v1[~keep] == 0)
+
+
+def test_set_threshold_reduces_to_fraction_mode(oracle):
+    """When every row holds exactly n magnitudes below tau, threshold mode is
+    fraction mode with frac = n/k, bit for bit."""
+    rng = np.random.default_rng(3)
+    L, k, d, n = 200, 32, 768, 5
+    W32 = (rng.uniform(0.2, 0.5, size=(L, k)) * rng.choice([-1, 1], size=(L, k))).astype(np.float32)
+    for l in range(L):
+        W32[l, rng.choice(k, size=n, replace=False)] = rng.uniform(-0.09, 0.09, size=n).astype(np.float32)
+    W = synth.f32_to_bf16_bits(W32)
+    I = synth.gen_indices(rng, L, k, d)
+    m = rng.standard_normal((L, k)).astype(np.float32)
+    v = rng.random((L, k)).astype(np.float32)
+    a = oracle.set_update_threshold(W, I, m, v, d, 0.1, seed=5, set_round=9)
+    b = oracle.set_update(W, I, m, v, d, n / k, seed=5, set_round=9)
+    for x, y in zip(a[:5], b[:5]):
+        assert np.array_equal(x, y)
+
+
+def test_set_threshold_extremes(oracle):
+    L, k, d = 50, 8, 40
+    W, I, m, v = make_state(23, L, k, d, "bf16")
+    W1, I1, _, _, mask, ex = oracle.set_update_threshold(W, I, m, v, d, 0.0, seed=1, set_round=1)
+    assert ex == 0 and mask.sum() == 0 and np.array_equal(I1, I) and np.array_equal(W1, W)
+    W1, I1, _, _, mask, ex = oracle.set_update_threshold(W, I, m, v, d, np.inf, seed=1, set_round=1)
+    assert ex == 0 and np.all(mask == 1) and np.all(W1 == 0)
+    for l in range(L):      # the whole row is new
+        assert not (set(I1[l].tolist()) & set(I[l].tolist())) and len(set(I1[l].tolist())) == k
