@@ -240,6 +240,20 @@ FFSL_API int ffsl_infer_topk(ffsl_layer *layer, const void *X, int32_t B, int32_
                     const int32_t *tgt_lab, int32_t nnz, float *p_at_k, void *workspace,
                     size_t workspace_bytes, void *stream);
 
+/* SET in threshold mode (the appendix's table of DST settings: prune mode
+ * "threshold" with a rewire threshold of 0.05 or 0.01): in every row, each
+ * slot with |W| < tau is pruned (compared as real numbers; a NaN weight is
+ * never below; tau = +inf prunes every finite weight), so the count n_l
+ * varies by row; n_l columns are then regrown exactly as in ffsl_set_update
+ * (same Philox stream, same acceptance rule, ascending slot order, W = m = v
+ * = 0).  A row that cannot find n_l new columns within 64*k + 4096 attempts
+ * (for instance n_l > d - k) is left unchanged and counted in
+ * *exhausted_out.  pruned_mask_out as in ffsl_set_update.
+ * Errors: FFSL_EINVAL if tau is negative or NaN. */
+FFSL_API int ffsl_set_update_threshold(ffsl_layer *layer, float tau, uint64_t seed,
+                    uint64_t set_round, uint8_t *pruned_mask_out, int32_t *exhausted_out,
+                    void *stream);
+
 /* Measurement hook: while both events are non-null, every sweep call
  * (ffsl_forward_loss, ffsl_backward, ffsl_train_step) records `start`
  * (a hipEvent_t) on its stream right before its main sweep kernel and `stop`

@@ -356,6 +356,15 @@ int ffsl_set_update(ffsl_layer *layer, float frac, uint64_t seed, uint64_t set_r
     return launch_set(ly, n, seed, set_round, pruned_mask_out, exhausted_out, static_cast<hipStream_t>(stream));
 }
 
+int ffsl_set_update_threshold(ffsl_layer *layer, float tau, uint64_t seed, uint64_t set_round,
+                              uint8_t *pruned_mask_out, int32_t *exhausted_out, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    if (!(tau >= 0.f)) return fail(FFSL_EINVAL, "tau must be >= 0 (got %g)", (double)tau);
+    return launch_set(layer->ly, 0, seed, set_round, pruned_mask_out, exhausted_out,
+                      static_cast<hipStream_t>(stream), true, tau + 0.f);
+}
+
 int ffsl_set_timing_events(ffsl_layer *layer, void *start, void *stop) {
     g_err.clear();
     if (!layer) return fail(FFSL_EINVAL, "layer is null");

@@ -121,8 +121,10 @@ bool sweep_wide_eligible(const Layer &ly, int mode);
 int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
                       float *dbp, int *grid_out, int *passes_out);
 int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
+// SET; in threshold mode (tau >= 0) every slot with |W| < tau is pruned and n
+// is ignored
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
-               uint8_t *mask, int32_t *exhausted, hipStream_t st);
+               uint8_t *mask, int32_t *exhausted, hipStream_t st, bool threshold = false, float tau = 0.f);
 int launch_validate(const Layer &ly, int32_t *bad_rows, hipStream_t st);
 int launch_adam_flat(void *p, int vt, const float *g, float *m, float *v, int64_t n, const AdamParams &ap,
                      int num_cu, hipStream_t st);

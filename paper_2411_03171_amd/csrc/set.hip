@@ -40,6 +40,10 @@ struct SetArgs {
     int32_t *exhausted;
     uint64_t seed, round;
     int64_t cap;
+    // threshold mode: prune every slot with |W| < tau (tau_bits = fp32 bits of
+    // tau >= 0; NaN weights are never below), so the count varies by row
+    int32_t threshold;
+    uint32_t tau_bits;
 };
 
 // LDS layout (32-bit words): bitmap [words][R], Itile [R][k+1], Wtile [R][kw+1]
@@ -53,7 +57,7 @@ template <int KM, int VT>
 __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
     extern __shared__ uint32_t lds[];
     const int R = a.R;
-    const int k = a.k, d = a.d, n = a.n;
+    const int k = a.k, d = a.d;
     const int kw = w_words<VT>(k);
     uint32_t *bitmap = lds;
     uint32_t *Itile = bitmap + (size_t)a.words * R;
@@ -132,7 +136,22 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
     }
 
     uint64_t pruned_lo = 0, pruned_hi = 0;  // slot bitmask, KM <= 128
-    if (n <= 4) {
+    int n = a.n;
+    if (a.threshold) {
+        // |W| < tau compared as fp32 bit patterns of non-negative values
+        n = 0;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+            if (j < k) {
+                const uint32_t mag = VT == FFSL_BF16 ? key[j] << 16 : key[j];
+                if (mag < a.tau_bits) {
+                    if (j < 64) pruned_lo |= 1ull << j;
+                    else pruned_hi |= 1ull << (j - 64);
+                    ++n;
+                }
+            }
+        }
+    } else if (n <= 4) {
         // the n smallest of the unique keys (|W| bits, slot) held in sorted
         // order by an insertion network of depth 4 over all k slots
         // bf16 keys (15 bits) and the slot fit one 32-bit word
@@ -169,7 +188,7 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
     // pass s-1.
     uint32_t pk = 0;
     int pj = -1;
-    for (int s = 0; s < (n <= 4 ? 0 : n); ++s) {
+    for (int s = 0; s < (a.threshold || n <= 4 ? 0 : n); ++s) {
         uint32_t bk = 0xffffffffu;
         int bj = KM;
 #pragma unroll
@@ -335,8 +354,10 @@ int set_launch_vt(const SetArgs &a, hipStream_t st) {
 }  // namespace
 
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_t *mask,
-               int32_t *exhausted, hipStream_t st) {
+               int32_t *exhausted, hipStream_t st, bool threshold, float tau) {
     SetArgs a{};
+    a.threshold = threshold ? 1 : 0;
+    a.tau_bits = threshold ? __builtin_bit_cast(uint32_t, tau) : 0u;
     a.L = ly.L;
     a.d = ly.d;
     a.k = ly.k;

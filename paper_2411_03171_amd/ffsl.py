@@ -36,6 +36,7 @@ SIGNATURES = {
     "ffsl_train_step_set": (_int, [_vp, _vp, _i32, _vp, _vp, _i32, _f32, _i64, _f32, _f32, _f32, _f32,
                                    _f32, _vp, _vp, _u32, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_set_update": (_int, [_vp, _f32, _u64, _u64, _vp, _vp, _vp]),
+    "ffsl_set_update_threshold": (_int, [_vp, _f32, _u64, _u64, _vp, _vp, _vp]),
     "ffsl_validate_indices": (_int, [_vp, _vp, _vp]),
     "ffsl_topk_workspace_bytes": (_sz, [_vp, _i32, _i32]),
     "ffsl_infer_topk": (_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
@@ -257,6 +258,18 @@ class SparseLayer:
         _check(load().ffsl_set_update(self._handle, float(frac), int(seed) & (2**64 - 1),
                                       int(set_round) & (2**64 - 1), _ptr(msk), _ptr(ex),
                                       _stream(torch)))
+        return msk, ex
+
+    def set_update_threshold(self, tau, seed, set_round, mask=True, exhausted_out=None):
+        """SET in threshold mode: prune every |W| < tau, regrow as many per row."""
+        torch = self.torch
+        msk = torch.empty((self.L, self.k), dtype=torch.uint8, device=self.W.device) if mask else None
+        ex = exhausted_out
+        if ex is None:
+            ex = torch.zeros(1, dtype=torch.int32, device=self.W.device)
+        _check(load().ffsl_set_update_threshold(self._handle, float(tau), int(seed) & (2**64 - 1),
+                                                int(set_round) & (2**64 - 1), _ptr(msk), _ptr(ex),
+                                                _stream(torch)))
         return msk, ex
 
     def set_timing_events(self, start, stop):
