@@ -246,6 +246,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--set-reps", type=int, default=10)
     ap.add_argument("--dense-reps", type=int, default=20)
+    ap.add_argument("--idx16-reps", type=int, default=10,
+                    help="timed steps and inference calls of the same layer with 16-bit indices (0 skips)")
     ap.add_argument("--infer-reps", type=int, default=10,
                     help="timed top-k inference calls (0 skips them)")
     ap.add_argument("--hinge-reps", type=int, default=10,
@@ -433,6 +435,48 @@ def main():
         print("[bench] inference top-%d: %.3f ms median, %.0f GB/s algorithmic (%.1f%% of HBM peak)" %
               (K_INF, inf_ms, inf_gbs, 100 * inf_gbs / HBM_PEAK_GBS), file=sys.stderr, flush=True)
 
+    # the same layer with 16-bit indices (2 bytes per slot less): the fused
+    # step and the inference call
+    idx16 = None
+    if args.idx16_reps > 0:
+        I16 = torch.from_numpy(inp.I.astype(np.uint16).view(np.int16)).to(dev)
+        layer16 = ffsl.SparseLayer(layer.W.clone(), I16, bias=layer.bias.clone(), B_max=w.B,
+                                   nnz_max=len(inp.lab), unfused=False).bind(w.d)
+        # the two layers' calls interleaved, so both medians come from the same
+        # stretch of time
+        t16 = 0
+        for _ in range(5):
+            t16 += 1
+            layer16.train_step(X, off, lab, t=t16, loss_out=loss, dX_out=dX)
+        st, st32 = [], []
+        for _ in range(args.idx16_reps):
+            t16 += 1
+            st.append(one_step(lambda: layer16.train_step(X, off, lab, t=t16, loss_out=loss, dX_out=dX)))
+            t += 1
+            st32.append(one_step(lambda: layer.train_step(X, off, lab, t=t, loss_out=loss, dX_out=dX)))
+        st16 = sorted(st)[len(st) // 2]
+        b16 = step_bytes - w.L * w.k * 2
+        idx16 = {"step_ms_median": st16, "step_algorithmic_bytes": b16,
+                 "step_achieved": b16 / (st16 * 1e-3) / 1e9,
+                 "int32_step_ms_median": sorted(st32)[len(st32) // 2]}
+        if infer is not None:
+            layer16.infer_topk(X, 5, off, lab, workspace=ws_inf)
+            torch.cuda.synchronize()
+            im16, im32 = [], []
+            for _ in range(args.idx16_reps):
+                im16.append(one_step(lambda: layer16.infer_topk(X, 5, off, lab, workspace=ws_inf)))
+                im32.append(one_step(lambda: layer.infer_topk(X, 5, off, lab, workspace=ws_inf)))
+            idx16["infer_ms_median"] = sorted(im16)[len(im16) // 2]
+            idx16["int32_infer_ms_median"] = sorted(im32)[len(im32) // 2]
+            idx16["infer_algorithmic_bytes"] = infer["algorithmic_bytes"] - w.L * w.k * 2
+        print("[bench] 16-bit indices: step %.3f ms (%.3f GB) vs %.3f ms int32; inference %s ms vs %s ms" %
+              (st16, b16 / 1e9, idx16["int32_step_ms_median"],
+               "%.3f" % idx16["infer_ms_median"] if "infer_ms_median" in idx16 else "-",
+               "%.3f" % idx16["int32_infer_ms_median"] if "infer_ms_median" in idx16 else "-"),
+              file=sys.stderr, flush=True)
+        del layer16, I16
+        torch.cuda.synchronize()
+
     dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
@@ -495,6 +539,7 @@ def main():
             "note": "FFSL_LOSS_SQHINGE; past_margin: bias -4, dW work skipped where a wave has no dlogit",
         },
         "infer_topk": infer,
+        "idx16": idx16,
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],
         "cpu_baseline": cpu,

@@ -53,6 +53,13 @@ typedef enum {
     FFSL_BF16 = 1  /* bfloat16 bit patterns (uint16); arithmetic in fp32    */
 } ffsl_dtype;
 
+typedef enum {
+    FFSL_IDX_I32 = 0,  /* int32 indices                                       */
+    FFSL_IDX_U16 = 1   /* uint16 indices, d <= 65536 (Sec. 2.2: 16-bit indices
+                          make the storage overhead of a sparse fp32 weight
+                          50 %; 2 bytes per slot less than int32)            */
+} ffsl_index_dtype;
+
 /* flags */
 #define FFSL_ACCUM_DX 1u   /* add into dX_out instead of overwriting it      */
 #define FFSL_ACCUM_LOSS 2u /* add into *loss_out instead of overwriting it   */
@@ -112,6 +119,18 @@ FFSL_API int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k
                       float *m, float *v, float *bias_m, float *bias_v,
                       float *dW, float *dbias, void *workspace,
                       size_t workspace_bytes, int32_t B_max, int32_t nnz_max);
+
+/* As ffsl_create_layer, with the index type given: index_dtype FFSL_IDX_I32
+ * (I is int32 [L,k]) or FFSL_IDX_U16 (I is uint16 [L,k], d <= 65536).  Every
+ * call on the layer reads and writes I in that type, with the same results
+ * as the int32 layer.  ffsl_create_layer is this call with FFSL_IDX_I32.
+ * (Every width this build accepts, d <= FFSL_MAX_D, fits 16 bits.)
+ * Errors: those of ffsl_create_layer; FFSL_EINVAL for another index_dtype. */
+FFSL_API int ffsl_create_layer_ex(ffsl_layer **out, int64_t L, int32_t d, int32_t k,
+                      int32_t value_dtype, int32_t index_dtype, void *W, void *I,
+                      float *bias, float *m, float *v, float *bias_m, float *bias_v,
+                      float *dW, float *dbias, void *workspace, size_t workspace_bytes,
+                      int32_t B_max, int32_t nnz_max);
 
 FFSL_API int ffsl_destroy_layer(ffsl_layer *layer);
 

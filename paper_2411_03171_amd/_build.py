@@ -39,10 +39,32 @@ def build(force: bool = True, verbose: bool = False) -> str:
             return LIB
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc] + HIPCC_FLAGS + ["-I", os.path.join(ROOT, "include"), "-o", tmp] + srcs
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    jobs = []
+    for src in srcs:
+        obj = os.path.join(objdir, os.path.basename(src)[:-4] + ".o")
+        jobs.append((src, obj, [hipcc] + compile_flags + ["-I", os.path.join(ROOT, "include"), "-c", "-o", obj, src]))
+    # one compiler process per source, a few at a time
+    workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", "8")), os.cpu_count() or 1))
+    pending = list(jobs)
+    running = []
+    while pending or running:
+        while pending and len(running) < workers:
+            src, obj, cmd = pending.pop(0)
+            if verbose:
+                print(" ".join(cmd), file=sys.stderr)
+            running.append((src, subprocess.Popen(cmd)))
+        src, proc = running.pop(0)
+        if proc.wait() != 0:
+            for _, other in running:
+                other.wait()
+            raise subprocess.CalledProcessError(proc.returncode, "hipcc " + src)
+    link = [hipcc, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + [obj for _, obj, _ in jobs]
     if verbose:
-        print(" ".join(cmd), file=sys.stderr)
-    subprocess.check_call(cmd)
+        print(" ".join(link), file=sys.stderr)
+    subprocess.check_call(link)
     os.replace(tmp, LIB)
     return LIB
 

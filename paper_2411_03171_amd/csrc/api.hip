@@ -155,10 +155,10 @@ size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max, int3
     return ws_layout(L, d, k, B_max, nnz_max, max_parts_for(cu)).total;
 }
 
-int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype, void *W,
-                      int32_t *I, float *bias, float *m, float *v, float *bias_m, float *bias_v, float *dW,
-                      float *dbias, void *workspace, size_t workspace_bytes, int32_t B_max,
-                      int32_t nnz_max) {
+int ffsl_create_layer_ex(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype,
+                         int32_t index_dtype, void *W, void *I, float *bias, float *m, float *v, float *bias_m,
+                         float *bias_v, float *dW, float *dbias, void *workspace, size_t workspace_bytes,
+                         int32_t B_max, int32_t nnz_max) {
     g_err.clear();
     if (!out) return fail(FFSL_EINVAL, "out is null");
     *out = nullptr;
@@ -166,6 +166,10 @@ int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t
     if (rc) return rc;
     if (value_dtype != FFSL_F32 && value_dtype != FFSL_BF16)
         return fail(FFSL_EINVAL, "value_dtype must be FFSL_F32 or FFSL_BF16");
+    if (index_dtype != FFSL_IDX_I32 && index_dtype != FFSL_IDX_U16)
+        return fail(FFSL_EINVAL, "index_dtype must be FFSL_IDX_I32 or FFSL_IDX_U16");
+    if (index_dtype == FFSL_IDX_U16 && d > 65536)
+        return fail(FFSL_EINVAL, "16-bit indices need d <= 65536 (got %d)", d);
     if (!W || !I || !m || !v) return fail(FFSL_EINVAL, "W, I, m and v are required");
     if (bias && (!bias_m || !bias_v)) return fail(FFSL_EINVAL, "bias needs bias_m and bias_v");
     if (dbias && !bias) return fail(FFSL_EINVAL, "dbias given without bias");
@@ -191,7 +195,8 @@ int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t
     ly.B_max = B_max;
     ly.nnz_max = nnz_max;
     ly.W = W;
-    ly.I = I;
+    ly.I = static_cast<int32_t *>(I);
+    ly.idx16 = index_dtype == FFSL_IDX_U16 ? 1 : 0;
     ly.bias = bias;
     ly.m = m;
     ly.v = v;
@@ -208,6 +213,14 @@ int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t
     ly.ev_stop = nullptr;
     *out = h;
     return FFSL_OK;
+}
+
+int ffsl_create_layer(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype, void *W,
+                      int32_t *I, float *bias, float *m, float *v, float *bias_m, float *bias_v, float *dW,
+                      float *dbias, void *workspace, size_t workspace_bytes, int32_t B_max,
+                      int32_t nnz_max) {
+    return ffsl_create_layer_ex(out, L, d, k, value_dtype, FFSL_IDX_I32, W, I, bias, m, v, bias_m, bias_v, dW,
+                                dbias, workspace, workspace_bytes, B_max, nnz_max);
 }
 
 int ffsl_destroy_layer(ffsl_layer *layer) {

@@ -15,7 +15,8 @@ struct Layer {
     int64_t L;
     int32_t d, k, vt, B_max, nnz_max;
     void *W;
-    int32_t *I;
+    int32_t *I;      // int32 [L,k], or uint16 [L,k] bit patterns when idx16
+    int idx16;       // 16-bit indices (d <= 65536)
     float *bias, *m, *v, *bm, *bv, *dW, *dbias;
     char *ws;
     size_t ws_bytes;

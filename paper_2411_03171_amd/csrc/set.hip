@@ -44,6 +44,7 @@ struct SetArgs {
     // tau >= 0; NaN weights are never below), so the count varies by row
     int32_t threshold;
     uint32_t tau_bits;
+    int32_t idx16;   // I holds uint16 indices
 };
 
 // LDS layout (32-bit words): bitmap [words][R], Itile [R][k+1], Wtile [R][kw+1]
@@ -71,7 +72,28 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
     {
         const uint32_t *Ig = reinterpret_cast<const uint32_t *>(a.I) + l0 * k;
         const int nI = rows * k;
-        if ((k & 3) == 0) {
+        if (a.idx16) {
+            const uint16_t *Ig16 = reinterpret_cast<const uint16_t *>(a.I) + l0 * k;
+            if ((k & 7) == 0) {
+                const uint4 *Ig4 = reinterpret_cast<const uint4 *>(Ig16);
+                for (int e8 = tid; e8 < nI / 8; e8 += R) {
+                    const uint4 q = Ig4[e8];
+                    const int e = 8 * e8, r = e / k, j = e - r * k;
+                    uint32_t *dst = Itile + r * (k + 1) + j;
+                    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        dst[2 * h] = w[h] & 0xffffu;
+                        dst[2 * h + 1] = w[h] >> 16;
+                    }
+                }
+            } else {
+                for (int e = tid; e < nI; e += R) {
+                    const int r = e / k, j = e - r * k;
+                    Itile[r * (k + 1) + j] = Ig16[e];
+                }
+            }
+        } else if ((k & 3) == 0) {
             const uint4 *Ig4 = reinterpret_cast<const uint4 *>(Ig);
             for (int e4 = tid; e4 < nI / 4; e4 += R) {
                 const uint4 q = Ig4[e4];
@@ -262,7 +284,10 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
                     if (r == q) c = acc[r];
                 ++q;
                 const int64_t o = l * k + j;
-                a.I[o] = c;
+                if (a.idx16)
+                    reinterpret_cast<uint16_t *>(a.I)[o] = (uint16_t)c;
+                else
+                    a.I[o] = c;
                 if constexpr (VT == FFSL_BF16)
                     static_cast<uint16_t *>(a.W)[o] = 0;
                 else
@@ -300,7 +325,8 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
 }
 
 template <int KM>
-__global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, int k, int d, int32_t *bad) {
+__global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, int k, int d, int32_t *bad,
+                                                  int idx16) {
     const int64_t l = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (l >= L) return;
     int idx[KM];
@@ -308,7 +334,7 @@ __global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, i
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
         if (j < k) {
-            idx[j] = I[l * k + j];
+            idx[j] = idx16 ? (int)reinterpret_cast<const uint16_t *>(I)[l * k + j] : I[l * k + j];
             ok = ok && idx[j] >= 0 && idx[j] < d;
         }
     }
@@ -365,6 +391,7 @@ int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_
     a.words = (ly.d + 31) / 32;
     a.W = ly.W;
     a.I = ly.I;
+    a.idx16 = ly.idx16;
     a.m = ly.m;
     a.v = ly.v;
     a.mask = mask;
@@ -378,13 +405,13 @@ int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_
 int launch_validate(const Layer &ly, int32_t *bad, hipStream_t st) {
     const int64_t blocks = (ly.L + 255) / 256;
     if (ly.k <= 16)
-        hipLaunchKernelGGL(k_validate<16>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+        hipLaunchKernelGGL(k_validate<16>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad, ly.idx16);
     else if (ly.k <= 32)
-        hipLaunchKernelGGL(k_validate<32>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+        hipLaunchKernelGGL(k_validate<32>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad, ly.idx16);
     else if (ly.k <= 64)
-        hipLaunchKernelGGL(k_validate<64>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+        hipLaunchKernelGGL(k_validate<64>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad, ly.idx16);
     else
-        hipLaunchKernelGGL(k_validate<128>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad);
+        hipLaunchKernelGGL(k_validate<128>, dim3((unsigned)blocks), dim3(256), 0, st, ly.I, ly.L, ly.k, ly.d, bad, ly.idx16);
     return check_launch("validate_indices");
 }
 

@@ -42,11 +42,32 @@ struct SweepArgs {
     float *dx_part;
     int want_loss;
     int hinge;   // squared hinge instead of BCE
+    int idx16;   // I holds uint16 indices
 };
 
 template <int KM>
-__device__ __forceinline__ void load_row_idx(const int32_t *I, int64_t l, int k, int d, int (&idx)[KM]) {
-    if (k == KM && (KM % 4) == 0) {
+__device__ __forceinline__ void load_row_idx(const int32_t *I, int64_t l, int k, int d, int (&idx)[KM],
+                                             bool idx16) {
+    if (idx16) {
+        // 16-bit indices
+        const uint16_t *I16 = reinterpret_cast<const uint16_t *>(I);
+        if (k == KM && (KM % 8) == 0) {
+            const uint4 *p = reinterpret_cast<const uint4 *>(I16 + l * KM);
+#pragma unroll
+            for (int q = 0; q < KM / 8; ++q) {
+                const uint4 t = p[q];
+                const uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    idx[8 * q + 2 * h] = (int)(w[h] & 0xffffu);
+                    idx[8 * q + 2 * h + 1] = (int)(w[h] >> 16);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < KM; ++j) idx[j] = (j < k) ? (int)I16[l * k + j] : 0;
+        }
+    } else if (k == KM && (KM % 4) == 0) {
         const int4 *p = reinterpret_cast<const int4 *>(I + l * KM);
 #pragma unroll
         for (int q = 0; q < KM / 4; ++q) {
@@ -150,7 +171,7 @@ __global__ void __launch_bounds__(SW_THREADS) k_sweep(const SweepArgs a) {
         float dw[KM];
         float bl = 0.f, db = 0.f;
         if (valid) {
-            load_row_idx<KM>(a.I, l, k, d, idx);
+            load_row_idx<KM>(a.I, l, k, d, idx, a.idx16 != 0);
             load_row_w<KM, VT>(a.W, l, k, w);
             if (a.bias) bl = a.bias[l];
         } else {
@@ -416,6 +437,7 @@ int launch_sweep(const SweepCall &c) {
     a.X = c.X;
     a.W = ly.W;
     a.I = ly.I;
+    a.idx16 = ly.idx16;
     a.bias = ly.bias;
     a.m = ly.m;
     a.v = ly.v;

@@ -47,6 +47,12 @@ __device__ __forceinline__ void stf2(Rsrc r, uint32_t off, float2 x) {
     __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
 }
 
+// a lane's two index words as loaded -> its two column indices: with 16-bit
+// indices both words hold the one word of the two slots
+__device__ __forceinline__ uint2 idx_pair(uint2 raw, int idx16) {
+    return idx16 ? make_uint2(raw.x & 0xffffu, raw.x >> 16) : raw;
+}
+
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
                                            false);

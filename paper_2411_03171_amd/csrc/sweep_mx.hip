@@ -75,6 +75,7 @@ struct MxArgs {
     // array sizes in bytes: the range of each buffer resource, and the offset
     // that the chunk loop uses for an access that must not happen
     uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    int32_t idx16;   // I holds uint16 indices
     // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
     // passes in dwp [L][32], dbp [L]
     int32_t b0, Btot;
@@ -115,7 +116,7 @@ __device__ __forceinline__ int swz(int r, int e) {
 }
 
 struct Prefetch {
-    uint2 iv;          // two index words of the chunk's I rows
+    uint2 iv;          // the lane's two index words as loaded (see idx_pair)
     uint32_t wv;       // one weight word of the chunk's W rows
     float2 m, v;       // moments of the lane's two slots (slot, slot + 1) of its row
     float b;           // its bias
@@ -129,9 +130,12 @@ __device__ __forceinline__ void prefetch(const MxArgs &a, const Rsrcs &R, int64_
                                          int slot, Prefetch &p) {
     const int64_t l0 = chunk * MX_NLAB;
     const bool live = chunk < a.nchunks;
-    const uint32_t oi = live ? (uint32_t)(l0 * MX_K * 4) + 8u * tid : a.nb_I;
-    const auto iv = __builtin_amdgcn_raw_buffer_load_b64(R.I, oi, 0, 0);
-    p.iv = make_uint2(iv[0], iv[1]);
+    // two word loads either way (no load reaches past the array): with 16-bit
+    // indices both read the one word that holds the lane's two slots
+    const uint32_t ish = a.idx16 ? 1u : 2u;   // log2 of the index bytes
+    const uint32_t oi = live ? ((uint32_t)(l0 * MX_K) << ish) + (2u << ish) * tid : a.nb_I;
+    const uint32_t w0 = ld32(R.I, oi), w1 = ld32(R.I, a.idx16 ? oi : oi + 4u);
+    p.iv = make_uint2(w0, w1);   // decoded where used (idx_pair), so the loads stay in flight
     const uint32_t ow = live ? (uint32_t)(l0 * MX_K * 2) + 4u * tid : a.nb_W;
     p.wv = ld32(R.W, ow);
     const int64_t l = l0 + lab;
@@ -289,7 +293,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
 
         // stage this chunk's rows: indices become clamped byte offsets of X columns
         {
-            const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
+            const uint2 ip = idx_pair(cur.iv, a.idx16);
+            const int i0 = min(max((int)ip.x, 0), d - 1), i1 = min(max((int)ip.y, 0), d - 1);
             *reinterpret_cast<int2 *>(Is + 2 * tid) = make_int2(i0 * MX_XS, i1 * MX_XS);
             Ws[tid] = cur.wv;
             if (!tg_lds && tid < MX_NLAB * 2) ym[tid] = 0u;
@@ -517,12 +522,17 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                     const int rowlane = lane & ~15;   // lane 0 of this row in the wave
                     const uint32_t n0c = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * (rowlane + min(r0, 15)), acol);
                     const uint32_t n1c = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * (rowlane + min(r1, 15)), acol);
-                    const uint32_t iw0 = ((sel >> s0) & 1u) ? n0c : cur.iv.x;
-                    const uint32_t iw1 = ((sel >> s1) & 1u) ? n1c : cur.iv.y;
-                    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-                    const u32x2 iw = {iw0, iw1};
-                    const uint32_t oi = valid ? (uint32_t)(l * MX_K + s0) * 4u : a.nb_I;
-                    __builtin_amdgcn_raw_buffer_store_b64(iw, R.I, oi, 0, 0);
+                    const uint2 ip = idx_pair(cur.iv, a.idx16);
+                    const uint32_t iw0 = ((sel >> s0) & 1u) ? n0c : ip.x;
+                    const uint32_t iw1 = ((sel >> s1) & 1u) ? n1c : ip.y;
+                    if (a.idx16) {
+                        st32(R.I, valid ? (uint32_t)(l * MX_K + s0) * 2u : a.nb_I, (iw0 & 0xffffu) | (iw1 << 16));
+                    } else {
+                        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                        const u32x2 iw = {iw0, iw1};
+                        const uint32_t oi = valid ? (uint32_t)(l * MX_K + s0) * 4u : a.nb_I;
+                        __builtin_amdgcn_raw_buffer_store_b64(iw, R.I, oi, 0, 0);
+                    }
                     const uint16_t mk = (uint16_t)(((sel >> s0) & 1u) | (((sel >> s1) & 1u) << 8));
                     __builtin_amdgcn_raw_buffer_store_b16(mk, R.mk, valid ? (uint32_t)(l * MX_K + s0) : a.nb_mask, 0, 0);
                 }
@@ -689,7 +699,8 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.nb_mask = c.set_mask ? (uint32_t)(ly.L * MX_K) : 0u;
     a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * MX_K * 2);
-    a.nb_I = (uint32_t)(ly.L * MX_K * 4);
+    a.idx16 = ly.idx16;
+    a.nb_I = (uint32_t)(ly.L * MX_K * (ly.idx16 ? 2 : 4));
     a.nb_m = (uint32_t)(ly.L * MX_K * 4);
     a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
     const int grid = (int)std::min<int64_t>(a.nchunks, std::min(ly.max_parts, ly.num_cu));

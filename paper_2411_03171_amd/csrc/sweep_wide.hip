@@ -71,6 +71,7 @@ struct WdArgs {
     // array sizes in bytes: the range of each buffer resource, and the offset
     // that the chunk loop uses for an access that must not happen
     uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    int32_t idx16;   // I holds uint16 indices
     // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
     // passes in dwp [L][64], dbp [L]
     int32_t b0, Btot;
@@ -91,7 +92,7 @@ __device__ __forceinline__ int qswz(int r, int e) {
 }
 
 struct Prefetch {
-    uint2 iv;          // two index words of the chunk's I rows
+    uint2 iv;          // the lane's two index words as loaded (see idx_pair)
     uint32_t wv;       // one weight word of the chunk's W rows
     float2 m, v;       // moments of the lane's two slots of its row
     float b;           // its bias
@@ -106,9 +107,12 @@ __device__ __forceinline__ void prefetch(const WdArgs &a, const Rsrcs &R, int64_
                                          int slot, Prefetch &p) {
     const int64_t l0 = chunk * WD_NLAB;
     const bool live = chunk < a.nchunks;
-    const auto iv = __builtin_amdgcn_raw_buffer_load_b64(R.I, live ? (uint32_t)(l0 * WD_K * 4) + 8u * tid : a.nb_I,
-                                                         0, 0);
-    p.iv = make_uint2(iv[0], iv[1]);
+    // two word loads either way (no load reaches past the array): with 16-bit
+    // indices both read the one word that holds the lane's two slots
+    const uint32_t ish = a.idx16 ? 1u : 2u;   // log2 of the index bytes
+    const uint32_t oi = live ? ((uint32_t)(l0 * WD_K) << ish) + (2u << ish) * tid : a.nb_I;
+    const uint32_t w0 = ld32(R.I, oi), w1 = ld32(R.I, a.idx16 ? oi : oi + 4u);
+    p.iv = make_uint2(w0, w1);   // decoded where used (idx_pair), so the loads stay in flight
     p.wv = ld32(R.W, live ? (uint32_t)(l0 * WD_K * 2) + 4u * tid : a.nb_W);
     const int64_t l = l0 + lab;
     const bool ok = live && l < a.L;
@@ -241,7 +245,8 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
 
         // stage this wave's rows: indices become clamped byte offsets of X columns
         {
-            const int i0 = min(max((int)cur.iv.x, 0), d - 1), i1 = min(max((int)cur.iv.y, 0), d - 1);
+            const uint2 ip = idx_pair(cur.iv, a.idx16);
+            const int i0 = min(max((int)ip.x, 0), d - 1), i1 = min(max((int)ip.y, 0), d - 1);
             *reinterpret_cast<int2 *>(Is + 2 * tid) = make_int2(i0 * WD_XS, i1 * WD_XS);
             reinterpret_cast<uint32_t *>(Ws)[tid] = cur.wv;
         }
@@ -511,7 +516,8 @@ int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part
     a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
     a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * WD_K * 2);
-    a.nb_I = (uint32_t)(ly.L * WD_K * 4);
+    a.idx16 = ly.idx16;
+    a.nb_I = (uint32_t)(ly.L * WD_K * (ly.idx16 ? 2 : 4));
     a.nb_m = (uint32_t)(ly.L * WD_K * 4);
     a.nb_b = ly.bias ? (uint32_t)(ly.L * 4) : 0u;
     const size_t shm = sweep_wide_lds(ly.d);

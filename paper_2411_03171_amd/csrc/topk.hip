@@ -50,6 +50,7 @@ struct TkArgs {
     int32_t thr_off;   // LDS byte offset of the per-sample shared bounds, then
                        // of the best score of each of the 32 lists per sample
     int32_t K;         // labels wanted per sample
+    int32_t idx16;     // I holds uint16 indices
     uint64_t *part;    // [B][nwg][KP] keys, sorted descending per list
 };
 
@@ -127,20 +128,33 @@ __device__ __forceinline__ void tk_load(const TkArgs &a, int64_t l0, int r, int 
     const int64_t base = l * a.k;
     const T *W = static_cast<const T *>(a.W);
     if ((a.k & 1) == 0) {
-        // even fan-in: the pair is one aligned load of indices and of weights
+        // even fan-in: the pair is two word loads (the same word twice with
+        // 16-bit indices) and one load of the weights
         if (s0 < a.k) {
-            out.c = *reinterpret_cast<const int2 *>(a.I + base + s0);
+            const uint32_t ish = a.idx16 ? 1u : 2u;
+            const char *ip = reinterpret_cast<const char *>(a.I) + ((size_t)(base + s0) << ish);
+            out.c.x = *reinterpret_cast<const int32_t *>(ip);
+            out.c.y = *reinterpret_cast<const int32_t *>(ip + (a.idx16 ? 0 : 4));
             out.w = *reinterpret_cast<const typename TkVal<VT>::Wp *>(W + base + s0);
         } else {
-            out.c = make_int2(a.d, a.d);
+            out.c = a.idx16 ? make_int2(a.d | (a.d << 16), 0) : make_int2(a.d, a.d);
             if constexpr (VT == FFSL_BF16)
                 out.w = 0u;
             else
                 out.w = make_float2(0.f, 0.f);
         }
     } else {
-        out.c.x = s0 < a.k ? a.I[base + s0] : a.d;
-        out.c.y = s0 + 1 < a.k ? a.I[base + s0 + 1] : a.d;
+        // odd fan-in: the two slots are loaded one by one and packed as an
+        // even fan-in's pair would be
+        const uint16_t *I16 = reinterpret_cast<const uint16_t *>(a.I);
+        if (a.idx16) {
+            const uint32_t c0 = s0 < a.k ? I16[base + s0] : (uint32_t)a.d;
+            const uint32_t c1 = s0 + 1 < a.k ? I16[base + s0 + 1] : (uint32_t)a.d;
+            out.c = make_int2((int)(c0 | (c1 << 16)), 0);
+        } else {
+            out.c.x = s0 < a.k ? a.I[base + s0] : a.d;
+            out.c.y = s0 + 1 < a.k ? a.I[base + s0 + 1] : a.d;
+        }
         if constexpr (VT == FFSL_BF16) {
             const uint32_t w0 = s0 < a.k ? W[base + s0] : 0u;
             const uint32_t w1 = s0 + 1 < a.k ? W[base + s0 + 1] : 0u;
@@ -160,11 +174,14 @@ struct TkRound {
 };
 
 template <int VT, int SPL>
-__device__ __forceinline__ TkRound<VT> tk_prep(const TkRaw<VT> &raw, int d) {
+__device__ __forceinline__ TkRound<VT> tk_prep(const TkRaw<VT> &raw, int d, int idx16) {
     constexpr int COL = 16 * SPL * (int)sizeof(typename TkVal<VT>::T);   // bytes per LDS column
+    // 16-bit indices: one word holds both slots
+    const uint32_t r0 = idx16 ? ((uint32_t)raw.c.x & 0xffffu) : (uint32_t)raw.c.x;
+    const uint32_t r1 = idx16 ? ((uint32_t)raw.c.x >> 16) : (uint32_t)raw.c.y;
     // indices outside [0,d) are clamped (the layer's precondition excludes
     // them); d itself is the zero column
-    const uint32_t c0 = min((uint32_t)raw.c.x, (uint32_t)d), c1 = min((uint32_t)raw.c.y, (uint32_t)d);
+    const uint32_t c0 = min(r0, (uint32_t)d), c1 = min(r1, (uint32_t)d);
     TkRound<VT> t;
     t.o0 = (int32_t)c0 * COL;
     t.o1 = (int32_t)c1 * COL;
@@ -354,7 +371,7 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
                 }
 
                 if (r == 0) zb = cur.bias;
-                const TkRound<VT> rd = tk_prep<VT, SPL>(cur, d);
+                const TkRound<VT> rd = tk_prep<VT, SPL>(cur, d, a.idx16);
                 const int npairs = min(16, (a.k - 32 * r + 1) >> 1);
                 if (npairs == 16)
                     tk_round_full<VT, SPL>(rd, xl, z);
@@ -624,6 +641,7 @@ int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_la
     a.X = X;
     a.W = ly.W;
     a.I = ly.I;
+    a.idx16 = ly.idx16;
     a.bias = ly.bias;
     a.L = ly.L;
     a.B = B;

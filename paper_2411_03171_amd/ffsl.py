@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libffsl.so")
 FFSL_OK, FFSL_EINVAL, FFSL_EUNSUPPORTED, FFSL_EHIP = 0, -1, -2, -3
 FFSL_F32, FFSL_BF16 = 0, 1
 FFSL_ACCUM_DX, FFSL_ACCUM_LOSS, FFSL_LOSS_SQHINGE = 1, 2, 4
+FFSL_IDX_I32, FFSL_IDX_U16 = 0, 1
 
 # (name, restype, argtypes) for every entry point of include/ffsl.h
 _i32, _i64, _u32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
@@ -27,6 +28,8 @@ SIGNATURES = {
     "ffsl_workspace_bytes": (_sz, [_i64, _i32, _i32, _i32, _i32]),
     "ffsl_create_layer": (_int, [ctypes.POINTER(_vp), _i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp, _sz, _i32, _i32]),
+    "ffsl_create_layer_ex": (_int, [ctypes.POINTER(_vp), _i64, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp,
+                                     _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i32, _i32]),
     "ffsl_destroy_layer": (_int, [_vp]),
     "ffsl_forward_loss": (_int, [_vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _u32, _vp]),
     "ffsl_backward": (_int, [_vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _u32, _vp]),
@@ -104,7 +107,8 @@ def footprint_bytes(L: int, k: int, value_bytes: int, bias: bool = True, unfused
 class SparseLayer:
     """A fixed fan-in layer whose state lives in torch tensors on the GPU.
 
-    State: W [L,k] (float32 or bfloat16), I [L,k] int32, bias [L] f32, Adam
+    State: W [L,k] (float32 or bfloat16), I [L,k] int32 (or 16-bit indices:
+    I given as int16 holding the uint16 bit patterns, d <= 65536), bias [L] f32, Adam
     moments m, v [L,k] f32 and bias_m, bias_v [L] f32; optional dW [L,k] and
     dbias [L] for the unfused path; a workspace sized by libffsl.
     """
@@ -128,7 +132,8 @@ class SparseLayer:
             raise TypeError("W must be float32 or bfloat16")
         f32 = dict(dtype=torch.float32, device=dev)
         self.W = W.contiguous()
-        self.I = I.to(device=dev, dtype=torch.int32).contiguous()
+        self.idx = FFSL_IDX_U16 if I.dtype == torch.int16 else FFSL_IDX_I32
+        self.I = I.to(device=dev, dtype=torch.int16 if self.idx == FFSL_IDX_U16 else torch.int32).contiguous()
         self.bias = bias.to(**f32).contiguous() if bias is not None else None
         self.m = m.to(**f32).contiguous() if m is not None else torch.zeros((L, k), **f32)
         self.v = v.to(**f32).contiguous() if v is not None else torch.zeros((L, k), **f32)
@@ -152,8 +157,8 @@ class SparseLayer:
             raise FfslError(FFSL_EINVAL, lib.ffsl_last_error().decode())
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.W.device)
         h = ctypes.c_void_p()
-        _check(lib.ffsl_create_layer(
-            ctypes.byref(h), self.L, self.d, self.k, self.vt, _ptr(self.W), _ptr(self.I),
+        _check(lib.ffsl_create_layer_ex(
+            ctypes.byref(h), self.L, self.d, self.k, self.vt, self.idx, _ptr(self.W), _ptr(self.I),
             _ptr(self.bias), _ptr(self.m), _ptr(self.v), _ptr(self.bias_m), _ptr(self.bias_v),
             _ptr(self.dW), _ptr(self.dbias), _ptr(self.workspace), nbytes, self.B_max,
             self.nnz_max))

@@ -1,6 +1,7 @@
 """Host-side checks of the C ABI (no GPU needed, no compute calls): the built
 library loads, exports every function include/ffsl.h declares, and the Python
 binding declares a signature for each of them."""
+import ctypes
 import os
 import re
 import subprocess
@@ -100,3 +101,19 @@ def test_paper_fanin_table_memory_slope():
     # fan-in 32 -> 64 -> 128: the slope equals the storage model to 1 %
     assert slopes[0] == pytest.approx(model, rel=0.01)
     assert slopes[1] == pytest.approx(model, rel=0.01)
+
+
+def test_create_layer_ex_rejects_bad_index_types(libpath):
+    """Argument checks of ffsl_create_layer_ex run on the host before any
+    device call: only two index types exist, and widths past the build's
+    limit (which 16-bit indices cover) are refused.  (The pointers are
+    placeholders; nothing is dereferenced.)"""
+    from paper_2411_03171_amd import ffsl
+    lib = ffsl.load()
+    h = ctypes.c_void_p()
+    p = ctypes.c_void_p(1 << 20)
+    args = lambda d, idx: (ctypes.byref(h), 1000, d, 32, ffsl.FFSL_BF16, idx, p, p, None, p, p, None, None,
+                           None, None, p, 1 << 30, 64, 64)
+    assert lib.ffsl_create_layer_ex(*args(70000, ffsl.FFSL_IDX_U16)) == ffsl.FFSL_EINVAL
+    assert lib.ffsl_create_layer_ex(*args(768, 7)) == ffsl.FFSL_EINVAL
+    assert b"index_dtype" in lib.ffsl_last_error()
