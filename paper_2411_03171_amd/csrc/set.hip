@@ -240,8 +240,11 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
         }
     }
 
-    // draws
-    int32_t acc[KM];
+    // draws.  The row's staged indices are in idx[] now, so its LDS row holds
+    // the accepted columns, each at the pruned slot it fills (pruned slots in
+    // ascending order); nothing reaches memory unless the row finds all n.
+    uint32_t *myrow = Itile + tid * (k + 1);
+    uint64_t fill_lo = pruned_lo, fill_hi = pruned_hi;   // pruned slots still empty
     int got = 0;
     uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
     for (int64_t att = 0; att < a.cap && got < n; ++att) {
@@ -259,9 +262,12 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
         const uint32_t bit = 1u << (c & 31);
         if (!(bw & bit)) {
             bw |= bit;
-#pragma unroll
-            for (int q = 0; q < KM; ++q)
-                if (q == got) acc[q] = c;
+            const int j = fill_lo ? __builtin_ctzll(fill_lo) : 64 + __builtin_ctzll(fill_hi);
+            if (fill_lo)
+                fill_lo &= fill_lo - 1;
+            else
+                fill_hi &= fill_hi - 1;
+            myrow[j] = (uint32_t)c;
             ++got;
         }
     }
@@ -272,30 +278,25 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
         return;
     }
 
-    int q = 0;
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-        if (j < k) {
-            const bool pr = j < 64 ? ((pruned_lo >> j) & 1ull) : ((pruned_hi >> (j - 64)) & 1ull);
-            if (pr) {
-                int32_t c = 0;
-#pragma unroll
-                for (int r = 0; r < KM; ++r)
-                    if (r == q) c = acc[r];
-                ++q;
-                const int64_t o = l * k + j;
-                if (a.idx16)
-                    reinterpret_cast<uint16_t *>(a.I)[o] = (uint16_t)c;
-                else
-                    a.I[o] = c;
-                if constexpr (VT == FFSL_BF16)
-                    static_cast<uint16_t *>(a.W)[o] = 0;
-                else
-                    static_cast<float *>(a.W)[o] = 0.f;
-                a.m[o] = 0.f;
-                a.v[o] = 0.f;
-            }
-        }
+    // write the pruned slots
+    for (uint64_t wl = pruned_lo, wh = pruned_hi; wl | wh;) {
+        const int j = wl ? __builtin_ctzll(wl) : 64 + __builtin_ctzll(wh);
+        if (wl)
+            wl &= wl - 1;
+        else
+            wh &= wh - 1;
+        const int32_t c = (int32_t)myrow[j];
+        const int64_t o = l * k + j;
+        if (a.idx16)
+            reinterpret_cast<uint16_t *>(a.I)[o] = (uint16_t)c;
+        else
+            a.I[o] = c;
+        if constexpr (VT == FFSL_BF16)
+            static_cast<uint16_t *>(a.W)[o] = 0;
+        else
+            static_cast<float *>(a.W)[o] = 0.f;
+        a.m[o] = 0.f;
+        a.v[o] = 0.f;
     }
     if (a.mask) {
         // k bytes per row, packed 4 per word when the row is word aligned
