@@ -15,8 +15,9 @@ oracle's own top-k where the sets agree.  Cases with exact ties (zero weights,
 so a score is its bias) must match the oracle label for label, including
 -inf and NaN scores.  Shapes: the largest label space's layout (fan-in 32, 64
 samples, width 768) in one and two batch tiles, fan-in 64 at width 2048, odd
-fan-in, a partial 32-slot round, fp32, ragged tiles, topk from 1 to 16, and
-topk = L."""
+fan-in, a partial 32-slot round, fp32, ragged tiles, topk from 1 to 16,
+topk = L, and label spaces large enough that more than 256 scan workgroups
+meet in the merge."""
 import numpy as np
 import pytest
 
@@ -37,9 +38,14 @@ CASES = {
     "k40_f32": synth.dataclasses.replace(synth.scaled(W1["c1_fp32_L4096"], L=901, B=70, d=256, k=40,
                                                       name="k40_f32")),
     "b1": synth.scaled(C4, L=513, B=1, name="b1"),
+    # one sample per lane (16-sample tiles) fits two scan workgroups per CU:
+    # with this many rows the merge takes more than 256 workgroup lists per
+    # sample
+    "c1_bigL": synth.scaled(W1["c1_fp32_L4096"], L=120000, B=16, name="c1_bigL"),
+    "b16_bigL": synth.scaled(C4, L=90000, B=16, d=256, name="b16_bigL"),
 }
 TOPKS = {"c4s": [1, 5, 8, 16], "c4s_b100": [5], "c3s": [3, 16], "c1": [5, 12], "odd_k7": [2, 9],
-         "k40_f32": [4], "b1": [1, 16]}
+         "k40_f32": [4], "b1": [1, 16], "c1_bigL": [4], "b16_bigL": [8]}
 
 
 @pytest.fixture(scope="module")
