@@ -142,7 +142,8 @@ def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
     p = lambda t: ctypes.c_void_p(t.data_ptr())
 
     def dense_step():
-        ffsl._check(lib.ffsl_dense_gelu_fwd(p(X), B, din, dout, p(W1), p(c), p(A), p(H), stream))
+        ffsl._check(lib.ffsl_dense_gelu_fwd(p(X), B, din, dout, p(W1), p(c), p(A), p(H), p(ws), ws.numel(),
+                                            stream))
         ffsl._check(lib.ffsl_dense_gelu_bwd(p(X), B, din, dout, p(W1), p(A), p(dH), p(dW1), p(dc), p(dX), 0,
                                             p(ws), ws.numel(), stream))
     us = median_us(dense_step)

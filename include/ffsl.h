@@ -296,7 +296,8 @@ FFSL_API int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out,
  * that will be used); calls sharing a workspace must be ordered.
  * ------------------------------------------------------------------------- */
 
-/* Workspace of ffsl_dense_gelu_bwd, or 0 for an invalid shape. */
+/* Workspace of ffsl_dense_gelu_fwd and ffsl_dense_gelu_bwd, or 0 for an
+ * invalid shape. */
 FFSL_API size_t ffsl_dense_workspace_bytes(int32_t B_max, int32_t din, int32_t dout);
 
 /* Wide intermediate layer between the encoder and the sparse classifier
@@ -304,10 +305,14 @@ FFSL_API size_t ffsl_dense_workspace_bytes(int32_t B_max, int32_t din, int32_t d
  * erf form):
  *   A[b,o] = c[o] + sum_i X[b,i] W1[i,o],   H[b,o] = A * Phi(A)
  *   X  [B,din] bf16;  W1 [din,dout] bf16;  c [dout] fp32, nullable
- *   A_out [B,dout] fp32 (kept for the backward);  H_out [B,dout] bf16 */
+ *   A_out [B,dout] fp32 (kept for the backward);  H_out [B,dout] bf16
+ *   workspace  nullable; with ffsl_dense_workspace_bytes(B, din, dout) bytes
+ *              the product is split over K so that small batches fill the
+ *              device (same result up to the order of the fp32 sums), and
+ *              without it it runs in one pass */
 FFSL_API int ffsl_dense_gelu_fwd(const void *X, int32_t B, int32_t din, int32_t dout,
                         const void *W1, const float *c, float *A_out, void *H_out,
-                        void *stream);
+                        void *workspace, size_t workspace_bytes, void *stream);
 
 /* Backward of ffsl_dense_gelu_fwd for the upstream gradient dH [B,dout]
  * fp32 (the sparse layer's dX):

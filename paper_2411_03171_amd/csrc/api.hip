@@ -439,7 +439,7 @@ size_t ffsl_dense_workspace_bytes(int32_t B_max, int32_t din, int32_t dout) {
 }
 
 int ffsl_dense_gelu_fwd(const void *X, int32_t B, int32_t din, int32_t dout, const void *W1, const float *c,
-                        float *A_out, void *H_out, void *stream) {
+                        float *A_out, void *H_out, void *workspace, size_t workspace_bytes, void *stream) {
     g_err.clear();
     int rc;
     if ((rc = check_dense_batch(B)) || (rc = check_width("din", din, 65536)) ||
@@ -447,8 +447,15 @@ int ffsl_dense_gelu_fwd(const void *X, int32_t B, int32_t din, int32_t dout, con
         (rc = check_aligned16("W1", W1)))
         return rc;
     if (!A_out || !H_out) return fail(FFSL_EINVAL, "A_out and H_out are required");
+    if (workspace) {
+        if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(FFSL_EINVAL, "workspace must be 256-byte aligned");
+        const size_t need = dense_ws(B, din, dout).total;
+        if (workspace_bytes < need)
+            return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    }
     return launch_dense_gelu_fwd(static_cast<const uint16_t *>(X), B, din, dout, static_cast<const uint16_t *>(W1),
-                                 c, A_out, static_cast<uint16_t *>(H_out), static_cast<hipStream_t>(stream));
+                                 c, A_out, static_cast<uint16_t *>(H_out), static_cast<char *>(workspace),
+                                 static_cast<hipStream_t>(stream));
 }
 
 int ffsl_dense_gelu_bwd(const void *X, int32_t B, int32_t din, int32_t dout, const void *W1, const float *A,

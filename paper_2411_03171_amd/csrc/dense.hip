@@ -2,7 +2,7 @@
 // Fig. 1 left): the wide intermediate layer H = GELU(X W1 + c) with its
 // backward, and the auxiliary cluster classifier Za = X Wa + ca with its BCE
 // loss and backward.  All products run on the matrix cores through one tiled
-// GEMM with fused epilogues:
+// GEMM (with a fused GELU epilogue for the intermediate layer):
 //
 //   C[M,N] = sum_k A(m,k) B(k,n),   A(m,k) = TA ? A[k*lda+m] : A[m*lda+k]
 //                                   B(k,n) = TB ? B[n*ldb+k] : B[k*ldb+n]
@@ -14,7 +14,8 @@
 // layout), and the next 128-deep tiles are loaded into registers while the
 // matrix cores work on the current ones.  Long K (the dX products) is split
 // over blockIdx.z into fp32 partials that a second kernel sums in a fixed
-// order.
+// order; so is the auxiliary head's forward, whose tiles alone would leave
+// most CUs idle, and its BCE runs in the kernel that sums the partials.
 #include <math.h>
 
 #include <algorithm>
@@ -32,7 +33,7 @@ constexpr int GT = 64;        // tile edge in M and N
 constexpr int GK = 128;       // K per stage
 constexpr int GKP = GK + 8;   // LDS row in elements (padded against bank conflicts)
 
-enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2, EPI_BCE = 3 };
+enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2 };
 
 struct GemmArgs {
     const uint16_t *A;
@@ -40,14 +41,9 @@ struct GemmArgs {
     const uint16_t *B;
     int64_t ldb;
     int M, N, K, kchunk;
-    float *C;                 // STORE: C[m*N+n]; PARTIAL: C[(z*M+m)*N+n]; GELU: pre-activation; BCE: dZ
-    const float *bias;        // GELU, BCE: per-column bias (nullable)
+    float *C;                 // STORE: C[m*N+n]; PARTIAL: C[(z*M+m)*N+n]; GELU: pre-activation
+    const float *bias;        // GELU: per-column bias (nullable)
     uint16_t *H;              // GELU: bf16 activation
-    const uint32_t *ymask;    // BCE: targets, one bit per (m, n), ywords words per row
-    int ywords;
-    float s;                  // BCE: loss scale
-    float *Zout;              // BCE: nullable logits
-    float *loss_part;         // BCE: one partial per workgroup
 };
 
 // One operand's 64-row x 128-deep tile in flight: four 16-byte groups per
@@ -147,7 +143,6 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
     }
 
     // accumulator element r of tile (mi, ni) is C[row 4*kq + r][column col]
-    float lsum = 0.f;
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -163,30 +158,12 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
                     g.C[o] = x;
                 } else if constexpr (EPI == EPI_PARTIAL) {
                     g.C[(int64_t)blockIdx.z * g.M * g.N + o] = x;
-                } else if constexpr (EPI == EPI_GELU) {
+                } else {
                     const float a = x + (g.bias ? g.bias[n] : 0.f);
                     g.C[o] = a;
                     g.H[o] = f32_to_bf16_bits(a * gelu_cdf(a));
-                } else {
-                    const float z = x + (g.bias ? g.bias[n] : 0.f);
-                    const float y = ((g.ymask[(int64_t)m * g.ywords + (n >> 5)] >> (n & 31)) & 1u) ? 1.f : 0.f;
-                    const float ex = expf(-fabsf(z));
-                    lsum += fmaxf(z, 0.f) - z * y + log1pf(ex);
-                    const float sig = z >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
-                    g.C[o] = g.s * (sig - y);
-                    if (g.Zout) g.Zout[o] = z;
                 }
             }
-    if constexpr (EPI == EPI_BCE) {
-        __shared__ float red[256];
-        red[tid] = lsum;
-        __syncthreads();
-        for (int st = 128; st > 0; st >>= 1) {
-            if (tid < st) red[tid] += red[tid + st];
-            __syncthreads();
-        }
-        if (tid == 0) g.loss_part[blockIdx.y * gridDim.x + blockIdx.x] = g.s * red[0];
-    }
 }
 
 // Column kernels: a workgroup owns 32 columns; its 8 row groups take every
@@ -211,33 +188,145 @@ __global__ void __launch_bounds__(256) k_gelu_bwd_cols(const float *A, const flo
     const int n = blockIdx.x * 32 + c;
     float sum = 0.f;
     if (n < N) {
-        for (int b = rg; b < B; b += 8) {
-            const int64_t o = (int64_t)b * N + n;
-            const float a = A[o];
-            const float pdf = 0.39894228040143268f * expf(-0.5f * a * a);
-            const float da = dH[o] * (gelu_cdf(a) + a * pdf);
-            dA16[o] = f32_to_bf16_bits(da);
-            sum += da;
+        // eight rows' loads in flight at a time
+        for (int b0 = rg; b0 < B; b0 += 64) {
+            float av[8], hv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int b = b0 + 8 * i;
+                av[i] = b < B ? A[(int64_t)b * N + n] : 0.f;
+                hv[i] = b < B ? dH[(int64_t)b * N + n] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int b = b0 + 8 * i;
+                if (b < B) {
+                    const float a = av[i];
+                    const float pdf = 0.39894228040143268f * expf(-0.5f * a * a);
+                    const float da = hv[i] * (gelu_cdf(a) + a * pdf);
+                    dA16[(int64_t)b * N + n] = f32_to_bf16_bits(da);
+                    sum += da;
+                }
+            }
         }
     }
     column_sum_out(red, sum, c, rg, n, N, dc);
 }
 
-// column sums of an fp32 [B,N] matrix (nullable) and its bf16 copy
-__global__ void __launch_bounds__(256) k_cols_cvt(const float *Z, int B, int N, uint16_t *Z16, float *csum) {
+// The auxiliary head's forward epilogue over split-K partials: per element
+// z = ca[c] + sum_s P[s][b][c] (ascending s), its BCE term and dlogit
+// g = s (sigmoid(z) - y); g is stored in bf16 for the two products and the
+// logits go to Zout when asked.  A workgroup takes 32 columns of one block of
+// 32 rows (blockIdx.y) and writes that block's column sums of g to
+// csum_part[blockIdx.y][.] and its loss sum to
+// loss_part[blockIdx.y * gridDim.x + blockIdx.x]; k_col_parts then adds the
+// blocks in order.
+constexpr int BCE_ROWS = 32;
+__global__ void __launch_bounds__(256) k_bce_cols(const float *P, int S, int B, int N, const float *bias,
+                                                  const int32_t *off, const int32_t *lab, float sc, uint16_t *G16,
+                                                  float *csum_part, float *Zout, float *loss_part) {
     __shared__ float red[8][33];
+    __shared__ float lred[256];
+    __shared__ uint32_t ym[BCE_ROWS];   // targets of the block's rows in this workgroup's 32 clusters
     const int c = threadIdx.x & 31, rg = threadIdx.x >> 5;
     const int n = blockIdx.x * 32 + c;
-    float sum = 0.f;
-    if (n < N) {
-        for (int b = rg; b < B; b += 8) {
-            const int64_t o = (int64_t)b * N + n;
-            const float z = Z[o];
-            Z16[o] = f32_to_bf16_bits(z);
-            sum += z;
+    const int64_t MN = (int64_t)B * N;
+    const int rb0 = blockIdx.y * BCE_ROWS, rb1 = min(B, rb0 + BCE_ROWS);
+    // cluster targets: bit c of ym[r] iff some positive l of sample rb0 + r has
+    // l mod N == blockIdx.x * 32 + c (negative labels are ignored)
+    if (threadIdx.x < BCE_ROWS) ym[threadIdx.x] = 0u;
+    __syncthreads();
+    {
+        const int e0 = off[rb0], e1 = off[rb1];
+        for (int e = e0 + (int)threadIdx.x; e < e1; e += 256) {
+            const int l = lab[e];
+            if (l < 0) continue;
+            const int cc = l % N - blockIdx.x * 32;
+            if (cc < 0 || cc >= 32) continue;
+            int r = 0;   // the sample of entry e: the last row with off[row] <= e
+            while (rb0 + r + 1 < rb1 && off[rb0 + r + 1] <= e) ++r;
+            atomicOr(&ym[r], 1u << cc);
         }
     }
-    column_sum_out(red, sum, c, rg, n, N, csum);
+    __syncthreads();
+    float sum = 0.f, lsum = 0.f;
+    if (n < N) {
+        const float bn = bias ? bias[n] : 0.f;
+        for (int b0 = rb0 + rg; b0 < rb1; b0 += 64) {
+            float zv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) zv[i] = 0.f;
+            for (int sp = 0; sp < S; ++sp) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int b = b0 + 8 * i;
+                    if (b < rb1) zv[i] += P[sp * MN + (int64_t)b * N + n];
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int b = b0 + 8 * i;
+                if (b < rb1) {
+                    const float z = zv[i] + bn;
+                    const float y = ((ym[b - rb0] >> c) & 1u) ? 1.f : 0.f;
+                    const float ex = expf(-fabsf(z));
+                    lsum += fmaxf(z, 0.f) - z * y + log1pf(ex);
+                    const float sig = z >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
+                    const float g = sc * (sig - y);
+                    const int64_t o = (int64_t)b * N + n;
+                    G16[o] = f32_to_bf16_bits(g);
+                    if (Zout) Zout[o] = z;
+                    sum += g;
+                }
+            }
+        }
+    }
+    lred[threadIdx.x] = lsum;
+    column_sum_out(red, sum, c, rg, n, N, csum_part + (int64_t)blockIdx.y * N);
+    for (int st = 128; st > 0; st >>= 1) {
+        if ((int)threadIdx.x < st) lred[threadIdx.x] += lred[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) loss_part[blockIdx.y * gridDim.x + blockIdx.x] = sc * lred[0];
+}
+
+// out[n] = sum_r part[r][n] over R row blocks, in order (out nullable); the
+// last workgroup also adds the nl loss partials into *loss (nullable)
+__global__ void __launch_bounds__(256) k_bce_finish(const float *part, int R, int N, float *out, const float *lpart,
+                                                    int nl, float *loss, int accum) {
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    if (n < N && out) {
+        float t = part[n];
+        for (int r = 1; r < R; ++r) t += part[(int64_t)r * N + n];
+        out[n] = t;
+    }
+    if (blockIdx.x == gridDim.x - 1 && loss) {
+        __shared__ float red[256];
+        float s = 0.f;
+        for (int i = threadIdx.x; i < nl; i += 256) s += lpart[i];
+        red[threadIdx.x] = s;
+        __syncthreads();
+        for (int st = 128; st > 0; st >>= 1) {
+            if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) *loss = (accum ? *loss : 0.f) + red[0];
+    }
+}
+
+// The intermediate layer's forward epilogue over split-K partials:
+// A = c + sum_s P[s] (ascending s), H = bf16(GELU(A))
+__global__ void __launch_bounds__(256) k_gelu_epi(const float *P, int S, int B, int N, const float *bias, float *A,
+                                                  uint16_t *H) {
+    const int64_t MN = (int64_t)B * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < MN; e += stride) {
+        float a = P[e];
+        for (int sp = 1; sp < S; ++sp) a += P[sp * MN + e];
+        a += bias ? bias[e % N] : 0.f;
+        A[e] = a;
+        H[e] = f32_to_bf16_bits(a * gelu_cdf(a));
+    }
 }
 
 // out[e] (+)= sum_z P[z][e], the split-K partials in ascending z
@@ -264,28 +353,6 @@ __global__ void __launch_bounds__(256) k_sum_partials(const float *part, int n, 
     if (threadIdx.x == 0) *loss = (accum ? *loss : 0.f) + red[0];
 }
 
-__global__ void __launch_bounds__(256) k_fill_u32(uint32_t *p, int64_t n, uint32_t x) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) p[e] = x;
-}
-
-// cluster targets: bit (b, l mod C) for every positive l of sample b; the
-// sample of CSR entry e is found by binary search in the offsets
-__global__ void __launch_bounds__(256) k_aux_targets(const int32_t *off, const int32_t *lab, int B, int nnz,
-                                                     int C, int words, uint32_t *ymask) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= nnz) return;
-    int lo = 0, hi = B;   // the last b with off[b] <= e
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (off[mid] <= e) lo = mid; else hi = mid;
-    }
-    const int l = lab[e];
-    if (l < 0) return;
-    const int c = l % C;
-    atomicOr(&ymask[(int64_t)lo * words + (c >> 5)], 1u << (c & 31));
-}
-
 template <bool TA, bool TB, int EPI>
 int gemm(const GemmArgs &g, int splits, hipStream_t st) {
     dim3 grid((g.N + GT - 1) / GT, (g.M + GT - 1) / GT, splits);
@@ -308,13 +375,29 @@ void split_k(int K, int *splits, int *kchunk) {
 
 int blocks_for(int64_t n) { return (int)std::min<int64_t>((n + 255) / 256, 4096); }
 
+// split count and K chunk of a forward product whose tiles alone would not
+// fill the device: enough splits for about 1024 workgroups, chunks of at
+// least 256
+void split_fwd(int K, int tiles, int *splits, int *kchunk) {
+    int s = std::max(1, std::min(K / 256, (1024 + tiles - 1) / tiles));
+    int kc = (K + s - 1) / s;
+    kc = (kc + GK - 1) / GK * GK;
+    s = (K + kc - 1) / kc;
+    *splits = s;
+    *kchunk = kc;
+}
+
 }  // namespace
 
 DenseWs dense_ws(int B_max, int din, int dout) {
     DenseWs w{};
     int S, kc;
     split_k(dout, &S, &kc);
+    int Sf, kcf;
+    split_fwd(din, ((dout + GT - 1) / GT) * ((B_max + GT - 1) / GT), &Sf, &kcf);
     size_t off = 0;
+    w.fwd_part = off;
+    off = al256(off + sizeof(float) * (size_t)Sf * B_max * dout);
     w.dA16 = off;
     off = al256(off + sizeof(uint16_t) * (size_t)B_max * dout);
     w.dx_part = off;
@@ -327,16 +410,17 @@ AuxWs aux_ws(int B_max, int d, int C) {
     AuxWs w{};
     int S, kc;
     split_k(C, &S, &kc);
-    const int words = (C + 31) / 32;
+    int Sf, kcf;
+    split_fwd(d, (C + GT - 1) / GT * ((B_max + GT - 1) / GT), &Sf, &kcf);
     size_t off = 0;
-    w.ymask = off;
-    off = al256(off + sizeof(uint32_t) * (size_t)B_max * words);
-    w.dz = off;
-    off = al256(off + sizeof(float) * (size_t)B_max * C);
+    w.zpart = off;
+    off = al256(off + sizeof(float) * (size_t)Sf * B_max * C);
     w.dz16 = off;
     off = al256(off + sizeof(uint16_t) * (size_t)B_max * C);
     w.loss_part = off;
-    off = al256(off + sizeof(float) * (size_t)((C + GT - 1) / GT) * ((B_max + GT - 1) / GT));
+    off = al256(off + sizeof(float) * (size_t)((C + 31) / 32) * ((B_max + 31) / 32));
+    w.csum_part = off;
+    off = al256(off + sizeof(float) * (size_t)((B_max + 31) / 32) * C);
     w.dx_part = off;
     off = al256(off + sizeof(float) * (size_t)S * B_max * d);
     w.total = off;
@@ -344,7 +428,7 @@ AuxWs aux_ws(int B_max, int d, int C) {
 }
 
 int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *c,
-                          float *A_out, uint16_t *H_out, hipStream_t st) {
+                          float *A_out, uint16_t *H_out, char *ws, hipStream_t st) {
     GemmArgs g{};
     g.A = X;
     g.lda = din;
@@ -353,11 +437,27 @@ int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uin
     g.M = B;
     g.N = dout;
     g.K = din;
-    g.kchunk = (din + GK - 1) / GK * GK;
-    g.C = A_out;
-    g.bias = c;
-    g.H = H_out;
-    return gemm<false, false, EPI_GELU>(g, 1, st);
+    const int tiles = ((dout + GT - 1) / GT) * ((B + GT - 1) / GT);
+    int S = 1, kc = din;
+    if (ws) split_fwd(din, tiles, &S, &kc);
+    if (S <= 1) {
+        // one pass with the GELU epilogue in the product
+        g.kchunk = (din + GK - 1) / GK * GK;
+        g.C = A_out;
+        g.bias = c;
+        g.H = H_out;
+        return gemm<false, false, EPI_GELU>(g, 1, st);
+    }
+    // split-K partials in the workspace, then the epilogue
+    const DenseWs w = dense_ws(B, din, dout);
+    float *P = reinterpret_cast<float *>(ws + w.fwd_part);
+    g.kchunk = kc;
+    g.C = P;
+    int rc = gemm<false, false, EPI_PARTIAL>(g, S, st);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_gelu_epi, dim3(blocks_for((int64_t)B * dout)), dim3(256), 0, st, P, S, B, dout, c, A_out,
+                       H_out);
+    return check_launch("gelu_epi");
 }
 
 int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *A,
@@ -406,22 +506,14 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, c
                    const int32_t *off, const int32_t *lab, int nnz, float s, float *loss, float *dWa, float *dca,
                    float *dX, float *Zout, bool accum_dx, bool accum_loss, char *ws, hipStream_t st) {
     const AuxWs w = aux_ws(B, d, C);
-    const int words = (C + 31) / 32;
-    uint32_t *ym = reinterpret_cast<uint32_t *>(ws + w.ymask);
-    float *dz = reinterpret_cast<float *>(ws + w.dz);
     uint16_t *dz16 = reinterpret_cast<uint16_t *>(ws + w.dz16);
     float *lp = reinterpret_cast<float *>(ws + w.loss_part);
-    const int64_t nm = (int64_t)B * words;
-    hipLaunchKernelGGL(k_fill_u32, dim3(blocks_for(nm)), dim3(256), 0, st, ym, nm, 0u);
-    int rc = check_launch("fill");
-    if (rc) return rc;
-    if (nnz > 0) {
-        hipLaunchKernelGGL(k_aux_targets, dim3((nnz + 255) / 256), dim3(256), 0, st, off, lab, B, nnz, C, words,
-                           ym);
-        rc = check_launch("aux_targets");
-        if (rc) return rc;
-    }
-    // Za = X Wa + ca with the BCE epilogue: A(m=b, k=i) = X[b*d+i], B(k=i, n=c) = Wa[i*C+c]
+    int rc;
+    // Za = X Wa + ca: split-K partials, A(m=b, k=i) = X[b*d+i], B(k=i, n=c) = Wa[i*C+c],
+    // then the BCE epilogue with the bf16 dlogits and their column sums
+    int Sf, kcf;
+    split_fwd(d, (C + GT - 1) / GT * ((B + GT - 1) / GT), &Sf, &kcf);
+    float *zp = reinterpret_cast<float *>(ws + w.zpart);
     GemmArgs g{};
     g.A = X;
     g.lda = d;
@@ -430,25 +522,22 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, c
     g.M = B;
     g.N = C;
     g.K = d;
-    g.kchunk = (d + GK - 1) / GK * GK;
-    g.C = dz;
-    g.bias = ca;
-    g.ymask = ym;
-    g.ywords = words;
-    g.s = s;
-    g.Zout = Zout;
-    g.loss_part = lp;
-    rc = gemm<false, false, EPI_BCE>(g, 1, st);
+    g.kchunk = kcf;
+    g.C = zp;
+    rc = gemm<false, false, EPI_PARTIAL>(g, Sf, st);
     if (rc) return rc;
-    const int nparts = ((C + GT - 1) / GT) * ((B + GT - 1) / GT);
-    if (loss) {
-        hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, st, lp, nparts, loss, accum_loss ? 1 : 0);
-        rc = check_launch("sum_partials");
+    const int eblocks = (C + 31) / 32, rblocks = (B + BCE_ROWS - 1) / BCE_ROWS;
+    float *cp = reinterpret_cast<float *>(ws + w.csum_part);
+    hipLaunchKernelGGL(k_bce_cols, dim3(eblocks, rblocks), dim3(256), 0, st, zp, Sf, B, C, ca, off, lab, s, dz16,
+                       cp, Zout, lp);
+    rc = check_launch("bce_cols");
+    if (rc) return rc;
+    if (dca || loss) {
+        hipLaunchKernelGGL(k_bce_finish, dim3((C + 255) / 256), dim3(256), 0, st, cp, rblocks, C, dca, lp,
+                           eblocks * rblocks, loss, accum_loss ? 1 : 0);
+        rc = check_launch("bce_finish");
         if (rc) return rc;
     }
-    hipLaunchKernelGGL(k_cols_cvt, dim3((C + 31) / 32), dim3(256), 0, st, dz, B, C, dz16, dca);
-    rc = check_launch("cols_cvt");
-    if (rc) return rc;
     // dWa[i,c] = sum_b X[b,i] dZ[b,c]
     GemmArgs h{};
     h.A = X;

@@ -158,23 +158,24 @@ int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_la
 
 // workspace of the intermediate layer's backward (byte offsets, 256-aligned)
 struct DenseWs {
+    size_t fwd_part; // fp32 [splits, B_max, dout] split-K partials of the forward
     size_t dA16;     // bf16 [B_max, dout]
     size_t dx_part;  // fp32 [splits, B_max, din]
     size_t total;
 };
 // workspace of the auxiliary head
 struct AuxWs {
-    size_t ymask;      // u32 [B_max, ceil(C/32)] cluster targets
-    size_t dz;         // fp32 [B_max, C]
-    size_t dz16;       // bf16 [B_max, C]
-    size_t loss_part;  // fp32, one per forward tile
+    size_t zpart;      // fp32 [splits, B_max, C] split-K partials of the logits
+    size_t dz16;       // bf16 [B_max, C] dlogits
+    size_t loss_part;  // fp32, one per epilogue workgroup (32 clusters x 32 samples)
+    size_t csum_part;  // fp32 [ceil(B_max/32), C] column sums of the dlogits per row block
     size_t dx_part;    // fp32 [splits, B_max, d]
     size_t total;
 };
 DenseWs dense_ws(int B_max, int din, int dout);
 AuxWs aux_ws(int B_max, int d, int C);
 int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *c,
-                          float *A_out, uint16_t *H_out, hipStream_t st);
+                          float *A_out, uint16_t *H_out, char *ws, hipStream_t st);
 int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *A,
                           const float *dH, float *dW1, float *dc, float *dX, bool accum, char *ws,
                           hipStream_t st);

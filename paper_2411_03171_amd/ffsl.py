@@ -334,8 +334,9 @@ def _workspace(torch, nbytes, dev):
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
 
 
-def dense_gelu_fwd(X, W1, c=None):
-    """H = GELU(X W1 + c) (bf16) and the pre-activation A (fp32) for the backward."""
+def dense_gelu_fwd(X, W1, c=None, split=True):
+    """H = GELU(X W1 + c) (bf16) and the pre-activation A (fp32) for the backward.
+    split=False runs the product in one pass (no workspace)."""
     import torch
     lib = load()
     _bf16_2d(X, "X")
@@ -344,8 +345,9 @@ def dense_gelu_fwd(X, W1, c=None):
     dout = W1.shape[1]
     A = torch.empty((B, dout), dtype=torch.float32, device=X.device)
     H = torch.empty((B, dout), dtype=torch.bfloat16, device=X.device)
-    _check(lib.ffsl_dense_gelu_fwd(_ptr(X), B, din, dout, _ptr(W1), _ptr(c), _ptr(A), _ptr(H),
-                                   _stream(torch)))
+    ws = _workspace(torch, lib.ffsl_dense_workspace_bytes(B, din, dout), X.device) if split else None
+    _check(lib.ffsl_dense_gelu_fwd(_ptr(X), B, din, dout, _ptr(W1), _ptr(c), _ptr(A), _ptr(H), _ptr(ws),
+                                   0 if ws is None else ws.numel(), _stream(torch)))
     return A, H
 
 

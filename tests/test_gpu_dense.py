@@ -60,10 +60,12 @@ def test_dense_gelu_fwd_bwd(torch_cuda, case):
     Xt, Wt = to_torch_values(X, "bf16", dev), to_torch_values(W1, "bf16", dev)
     ct = torch.from_numpy(c).to(dev)
     note("dense gelu fwd %s B=%d din=%d dout=%d" % (name, B, din, dout))
-    A, H = ffsl.dense_gelu_fwd(Xt, Wt, ct)
-    torch.cuda.synchronize()
-    assert_close(A.cpu().numpy(), A_ref, RTOL_F32, "A")
-    assert_close(H.float().cpu().numpy(), H_ref, RTOL_BF16, "H")
+    # the product split over K (with a workspace) and in one pass
+    for split in (True, False):
+        A, H = ffsl.dense_gelu_fwd(Xt, Wt, ct, split=split)
+        torch.cuda.synchronize()
+        assert_close(A.cpu().numpy(), A_ref, RTOL_F32, "A (split=%s)" % split)
+        assert_close(H.float().cpu().numpy(), H_ref, RTOL_BF16, "H (split=%s)" % split)
     # backward from the same pre-activation on both sides
     A32 = A_ref.astype(np.float32)
     dW1_ref, dc_ref, dX_ref = oracle.dense_gelu_bwd(_f64(X), _f64(W1), A32.astype(np.float64),
