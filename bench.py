@@ -182,6 +182,67 @@ def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
     return out
 
 
+def time_composed(torch, ffsl, synth, ev, stream, dev, reps, seed):
+    """One whole training step of each workload with dense parts, through
+    paper_2411_03171_amd.model: the intermediate layer + sparse layer at the C3
+    sizes, the sparse layer + auxiliary head at the C5 sizes (Adam on every
+    parameter, no SET).  Each is timed with HIP events around the step (median
+    of `reps`), next to the same sparse layer's step alone on an input of its
+    width, so the dense parts' share is visible."""
+    import numpy as np
+    from paper_2411_03171_amd.model import Model
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def median_ms(fn):
+        for t in range(1, 4):
+            fn(t)
+        torch.cuda.synchronize()
+        ms = []
+        for t in range(4, 4 + reps):
+            a, b = ev.create(), ev.create()
+            ev.record(a, stream)
+            fn(t)
+            ev.record(b, stream)
+            torch.cuda.synchronize()
+            ms.append(ev.elapsed_ms(a, b))
+            ev.destroy(a)
+            ev.destroy(b)
+        return sorted(ms)[len(ms) // 2]
+
+    out = {}
+    for name in ("c3_inter2048_L1M", "c5_aux8192_L1M"):
+        w = synth.WORKLOADS[name]
+        print("[bench] composed step %s: generating" % name, file=sys.stderr, flush=True)
+        inp = synth.make_layer_inputs(w, seed)
+        layer = ffsl.SparseLayer(bf(inp.W), torch.from_numpy(inp.I).to(dev),
+                                 bias=torch.from_numpy(inp.bias).to(dev), B_max=w.B, nnz_max=len(inp.lab),
+                                 unfused=False).bind(w.d)
+        X = bf(inp.X)
+        off = torch.from_numpy(inp.off.astype(np.int32)).to(dev)
+        lab = torch.from_numpy(inp.lab).to(dev)
+        if w.din:
+            model = Model(layer, W1=bf(synth.make_intermediate(w, seed)), c=torch.zeros(w.d, device=dev))
+            Xs = bf(synth.gen_x(np.random.default_rng(seed + 1), w.B, w.d, "layernorm", "bf16"))
+        else:
+            model = Model(layer, Wa=bf(synth.make_aux(w, seed)), ca=torch.zeros(w.aux_clusters, device=dev),
+                          aux_w0=1.0, aux_cutoff_epoch=None)
+            Xs = X
+        ms = median_ms(lambda t: model.train_step(X, off, lab, t))
+        ms_sparse = median_ms(lambda t: layer.train_step(Xs, off, lab, t))
+        out[name] = {"ms_median": ms, "sparse_ms_median": ms_sparse, "dense_parts_ms": ms - ms_sparse,
+                     "value": w.B * w.L / (ms * 1e-3), "unit": "sample*labels/s",
+                     "shape": {"L": w.L, "k": w.k, "B": w.B, "d": w.d, "din": w.din,
+                               "aux_clusters": w.aux_clusters}}
+        print("[bench] composed step %s: %.3f ms (sparse layer alone %.3f ms)" % (name, ms, ms_sparse),
+              file=sys.stderr, flush=True)
+        layer.close()
+        del model, layer, X, Xs
+        torch.cuda.synchronize()
+    return out
+
+
 def cpu_baseline(w, inp, target_s=12.0):
     """The oracle (float64, single thread) on the first L' label rows of the
     same workload: one fused step (forward, BCE, backward, Adam)."""
@@ -254,6 +315,8 @@ def main():
     ap.add_argument("--hinge-reps", type=int, default=10,
                     help="squared hinge steps per case (0 skips them, e.g. under a kernel trace "
                          "whose per-kernel average should cover the BCE step only)")
+    ap.add_argument("--composed-reps", type=int, default=5,
+                    help="whole steps of the workloads with dense parts, each (0 skips them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sparse-only", action="store_true",
                     help="for a workload with dense parts, time its sparse layer alone (at the "
@@ -482,6 +545,10 @@ def main():
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
 
+    composed = None
+    if args.composed_reps > 0:
+        composed = time_composed(torch, ffsl, synth, ev, stream, dev, args.composed_reps, args.seed)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
@@ -543,6 +610,7 @@ def main():
         "idx16": idx16,
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],
+        "composed_step": composed,
         "cpu_baseline": cpu,
         "loss": final_loss,
     }

@@ -1,0 +1,197 @@
+"""GPU parity of one composed training step (paper_2411_03171_amd.model) against
+the same composition of oracle calls on the same seeded inputs: the
+intermediate GELU layer in front of the sparse layer (its forward, the sparse
+step on its bf16 output, its backward from the sparse layer's dX, Adam on W1
+and c), and the auxiliary cluster head beside it (loss and dX added with the
+scheduled weight, Adam on Wa and ca), with a SET update when the schedule says
+one is due.  The dense parameters start from non-zero Adam moments, so that an
+error in a gradient shows in m and in the update."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2411_03171_amd import schedule, synth
+from tests.parity import (RTOL_BF16, RTOL_F32, assert_close, batch_to_gpu, from_torch_bits, make_gpu_layer,
+                          note, to_torch_values, values_f64)
+
+pytestmark = pytest.mark.gpu
+
+W1_ = synth.WORKLOADS
+C3S = synth.scaled(W1_["c3_inter2048_L1M"], L=901, B=24, d=128, name="c3s_model")
+C3S = synth.dataclasses.replace(C3S, din=96)
+C5S = synth.dataclasses.replace(synth.scaled(W1_["c5_aux8192_L1M"], L=1003, B=24, d=128, name="c5s_model"),
+                                aux_clusters=40)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2411_03171_amd import ffsl
+    ffsl.load()
+    return torch
+
+
+def _f64(bits):
+    return synth.bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def _moments(rng, shape):
+    return ((rng.standard_normal(shape) * 1e-3).astype(np.float32),
+            (rng.random(shape) * 1e-5).astype(np.float32))
+
+
+def _check_param(got, ref, g_ref, m_ref, v_ref, t, lr, is_bf16, what, b1=0.9, b2=0.999, eps=1e-8):
+    """The parameter after Adam against the oracle's.  The gradients went
+    through bf16 operands, so each may be off by up to RTOL_BF16 of its
+    tensor's largest entry (dg); the update lr * mh / (sqrt(vh) + eps) then
+    moves by at most its first-order change through m ((1-b1) dg) and v
+    ((1-b2) 2 |g| dg), taken with a factor 1.5; a bf16 parameter adds one
+    rounding of the stored value."""
+    got = np.asarray(got, dtype=np.float64)
+    dg = RTOL_BF16 * np.abs(g_ref).max()
+    bc1, bc2 = 1.0 - b1 ** t, 1.0 - b2 ** t
+    mh, vh = m_ref / bc1, v_ref / bc2
+    sv = np.sqrt(vh)
+    den = sv + eps
+    d_m = (1.0 - b1) * dg / bc1 / den
+    d_v = np.abs(mh) * (1.0 - b2) * 2.0 * np.abs(g_ref) * dg / bc2 / np.maximum(2.0 * sv * den * den, 1e-300)
+    allow = 1.5 * lr * (d_m + d_v) + 1e-6 * np.abs(ref) + 1e-12
+    if is_bf16:
+        big = np.maximum(np.abs(got), np.abs(ref))
+        allow = allow + np.exp2(np.floor(np.log2(np.maximum(big, 1e-30))) - 8)
+    bad = np.abs(got - ref) > allow
+    assert not bad.any(), (what, int(bad.sum()), float(np.abs(got - ref)[bad].max()))
+
+
+def _sparse_ref(layer_in, w, H, bias, off, lab, m0, v0, t, lr, wd):
+    Wv = values_f64(layer_in.W, w.value)
+    L = Wv.shape[0]
+    return oracle.train_step(H, Wv, layer_in.I, bias.astype(np.float64), m0.astype(np.float64),
+                             v0.astype(np.float64), np.zeros(L), np.zeros(L), off, lab, 1.0 / H.shape[0], t,
+                             lr=lr, wd=wd, w_bf16=(w.value == "bf16"))
+
+
+def test_model_intermediate_layer_step(torch_cuda):
+    torch = torch_cuda
+    from paper_2411_03171_amd import ffsl
+    from paper_2411_03171_amd.model import Model
+    w = C3S
+    inp = synth.make_layer_inputs(w, 5)        # X is [B, din]
+    rng = np.random.default_rng(31)
+    W1 = synth.make_dense(rng, w.din, w.d)
+    c = (rng.standard_normal(w.d) * 0.1).astype(np.float32)
+    bias = (rng.standard_normal(w.L) * 0.1).astype(np.float32)
+    m0, v0 = _moments(rng, (w.L, w.k))
+    mW0, vW0 = _moments(rng, (w.din, w.d))
+    mc0, vc0 = _moments(rng, (w.d,))
+    t, lr, wd, lr_i = 3, 1e-2, 1e-4, 2e-3
+
+    # the oracle composition
+    X = _f64(inp.X)
+    A_ref, H_ref = oracle.dense_gelu_fwd(X, _f64(W1), c.astype(np.float64))
+    H16 = oracle.bf16_to_f64(oracle.round_bf16(H_ref))     # the sparse layer reads H in bf16
+    r = _sparse_ref(inp, w, H16, bias, inp.off, inp.lab, m0, v0, t, lr, wd)
+    dW1, dc, dXe = oracle.dense_gelu_bwd(X, _f64(W1), A_ref, r["dX"])
+    W1n, mW1n, vW1n = oracle.adam(_f64(W1), mW0, vW0, dW1, t, lr=lr_i)
+    cn, mcn, vcn = oracle.adam(c.astype(np.float64), mc0, vc0, dc, t, lr=lr_i)
+
+    dev = "cuda:0"
+    note("model step: intermediate layer B=%d din=%d d=%d L=%d" % (w.B, w.din, w.d, w.L))
+    layer = make_gpu_layer(inp, w, bias_values=bias, unfused=False)
+    layer.m.copy_(torch.from_numpy(m0))
+    layer.v.copy_(torch.from_numpy(v0))
+    W1t = to_torch_values(W1, "bf16", dev)
+    ct = torch.from_numpy(c).to(dev)
+    model = Model(layer, W1=W1t, c=ct, lr=lr, wd=wd, lr_inter=lr_i)
+    for a, b in ((model.mW1, mW0), (model.vW1, vW0), (model.mc, mc0), (model.vc, vc0)):
+        a.copy_(torch.from_numpy(b))
+    Xt, offt, labt = batch_to_gpu(inp.X, inp.off, inp.lab, "bf16")
+    loss, dX, mask = model.train_step(Xt, offt, labt, t)
+    torch.cuda.synchronize()
+    assert mask is None
+    assert_close(np.array([float(loss.cpu()[0])]), np.array([r["loss"]]), RTOL_BF16, "loss")
+    assert_close(dX.cpu().numpy(), dXe, RTOL_BF16, "dX of the features")
+    assert_close(model.mW1.cpu().numpy(), mW1n, RTOL_BF16, "m of W1")
+    assert_close(model.vW1.cpu().numpy(), vW1n, 2 * RTOL_BF16, "v of W1")
+    assert_close(model.mc.cpu().numpy(), mcn, RTOL_BF16, "m of c")
+    _check_param(model.W1.float().cpu().numpy(), W1n, dW1, mW1n, vW1n, t, lr_i, True, "W1")
+    _check_param(model.c.cpu().numpy(), cn, dc, mcn, vcn, t, lr_i, False, "c")
+    assert_close(layer.m.cpu().numpy(), r["m"], RTOL_BF16, "m of the sparse layer")
+    _check_param(values_f64(from_torch_bits(layer.W, "bf16"), "bf16"), r["W"], r["dW"], r["m"], r["v"], t, lr,
+                 True, "sparse W")
+
+
+@pytest.mark.parametrize("epoch,set_step", [(0.25, False), (0.5, True), (2.0, False)],
+                         ids=["aux_early", "aux_mid_set", "past_cutoff"])
+def test_model_aux_head_step(torch_cuda, epoch, set_step):
+    torch = torch_cuda
+    from paper_2411_03171_amd.model import Model
+    w = C5S
+    inp = synth.make_layer_inputs(w, 6)
+    rng = np.random.default_rng(37)
+    C = w.aux_clusters
+    Wa = synth.make_dense(rng, w.d, C)
+    ca = (rng.standard_normal(C) * 0.1).astype(np.float32)
+    bias = (rng.standard_normal(w.L) * 0.1).astype(np.float32)
+    m0, v0 = _moments(rng, (w.L, w.k))
+    mA0, vA0 = _moments(rng, (w.d, C))
+    mc0, vc0 = _moments(rng, (C,))
+    lr, wd, lr_a, w0, cut = 1e-2, 0.0, 5e-3, 0.7, 1.5
+    interval, total = 4, 10
+    t = 4 if set_step else 3
+    assert schedule.set_due(t, interval, total) == set_step
+    wgt = schedule.aux_weight(epoch, w0, cut)
+
+    X = _f64(inp.X)
+    r = _sparse_ref(inp, w, X, bias, inp.off, inp.lab, m0, v0, t, lr, wd)
+    loss_ref, dX_ref = r["loss"], r["dX"].copy()
+    if wgt > 0:
+        a = oracle.aux_bce(X, _f64(Wa), ca.astype(np.float64), inp.off, inp.lab, wgt / w.B)
+        loss_ref += a["loss"]
+        dX_ref += a["dXa"]
+        Wan, mAn, vAn = oracle.adam(_f64(Wa), mA0, vA0, a["dWa"], t, lr=lr_a)
+        can, mcn, vcn = oracle.adam(ca.astype(np.float64), mc0, vc0, a["dca"], t, lr=lr_a)
+    if set_step:
+        Wb = oracle.round_bf16(r["W"])
+        Wset, Iset, mset, vset, mask_ref, _ = oracle.set_update(Wb, inp.I, r["m"], r["v"], w.d, 0.25, 77,
+                                                                schedule.set_round(t, interval))
+
+    dev = "cuda:0"
+    note("model step: aux head epoch=%g set=%s B=%d d=%d C=%d L=%d" % (epoch, set_step, w.B, w.d, C, w.L))
+    layer = make_gpu_layer(inp, w, bias_values=bias, unfused=False)
+    layer.m.copy_(torch.from_numpy(m0))
+    layer.v.copy_(torch.from_numpy(v0))
+    Wat = to_torch_values(Wa, "bf16", dev)
+    cat = torch.from_numpy(ca).to(dev)
+    model = Model(layer, Wa=Wat, ca=cat, lr=lr, wd=wd, lr_aux=lr_a, set_frac=0.25, set_interval=interval,
+                  total_steps=total, set_seed=77, aux_w0=w0, aux_cutoff_epoch=cut)
+    for x, y in ((model.mWa, mA0), (model.vWa, vA0), (model.mca, mc0), (model.vca, vc0)):
+        x.copy_(torch.from_numpy(y))
+    Xt, offt, labt = batch_to_gpu(inp.X, inp.off, inp.lab, "bf16")
+    loss, dX, mask = model.train_step(Xt, offt, labt, t, epoch=epoch)
+    torch.cuda.synchronize()
+    assert_close(np.array([float(loss.cpu()[0])]), np.array([loss_ref]), RTOL_BF16, "loss")
+    assert_close(dX.cpu().numpy(), dX_ref, RTOL_BF16, "dX of the features")
+    if wgt > 0:
+        assert_close(model.mWa.cpu().numpy(), mAn, RTOL_BF16, "m of Wa")
+        _check_param(model.Wa.float().cpu().numpy(), Wan, a["dWa"], mAn, vAn, t, lr_a, True, "Wa")
+        _check_param(model.ca.cpu().numpy(), can, a["dca"], mcn, vcn, t, lr_a, False, "ca")
+    else:
+        # past the cut-off the head does not run: its parameters stay as they were
+        np.testing.assert_array_equal(from_torch_bits(model.Wa, "bf16"), Wa)
+        np.testing.assert_array_equal(model.mWa.cpu().numpy(), mA0)
+    if set_step:
+        # the topology update follows the step: compare what is decided by the
+        # draw stream and the pruned magnitudes (the bf16 weights can differ by
+        # one rounding from the oracle's, so only rows whose pruned set is the
+        # same are compared index for index)
+        assert mask is not None
+        Ig = layer.I.cpu().numpy()
+        same = np.all(mask.cpu().numpy() == mask_ref, axis=1)
+        assert same.mean() > 0.95, same.mean()
+        np.testing.assert_array_equal(Ig[same], Iset[same])
+        assert np.all(np.diff(np.sort(Ig, axis=1), axis=1) > 0)
+    else:
+        assert mask is None
+        np.testing.assert_array_equal(layer.I.cpu().numpy(), inp.I)
