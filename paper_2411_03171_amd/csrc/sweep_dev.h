@@ -81,6 +81,7 @@ constexpr int DPP_ROW_MIRROR = 0x140;       // lane j <- 15 - j within 16
 constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane j <- 7 - j within 8
 constexpr int DPP_QUAD_3210 = 0x1B;         // lane j <- j ^ 3 within 4
 constexpr int DPP_QUAD_1032 = 0xB1;         // lane j <- j ^ 1 within 4
+constexpr int DPP_ROW_ROR8 = 0x128;        // lane j <- j ^ 8 within 16 (rotation by 8)
 
 // Slot key of lane j of a 16-lane group in the dW reduce-scatter over 32
 // slots: the lane keeps slot r ^ (lane_key(j) with bit 1 cleared) in register

@@ -9,8 +9,9 @@
 // sweep over the [L,k] arrays:
 //
 // Workgroup: 512 threads (8 waves), one per CU, persistent over chunks of 16
-// label rows.  Thirty-two lanes serve one row: lane u handles sample
-// b = u & 15 of the pass and the half h = u >> 4 of the row's 64 slots.
+// label rows.  Thirty-two lanes serve one row: lane u handles the four
+// samples 4q .. 4q+3 of the pass, q = u >> 3, and the eight slots
+// 8g .. 8g+7 of the row, g = u & 7.
 //
 //   LDS  Xs [d][16] bf16   the pass's samples transposed (column i is 32
 //                          contiguous bytes), zero-padded past the pass
@@ -21,14 +22,16 @@
 //                          and weight rows; each wave stages its own two rows
 //        tg                the pass's positives as sorted (label, sample) keys
 //
-//   1. gather: for each of its 32 slots the lane reads the 2 bytes
-//      X[b, I[l,j]], two slots packed per register: the pairs line up with
-//      the row's weight pairs, so the forward is one v_dot2 per slot pair,
-//      and the halves' partial sums meet with one v_permlane16_swap;
-//   2. BCE loss and dlogit g of (row, sample);
-//   3. dW: one v_dot2 per slot (g rounded to bf16) and the 16-lane
-//      reduce-scatter over the pass's samples (register r holds slot
-//      r ^ Kp(b) of the half; the lane keeps two slots);
+//   1. gather: for each of its 8 slots the lane reads the 8 bytes
+//      X[4q .. 4q+3, I[l,j]]; the sample pairs are repacked into slot pairs
+//      with v_perm and reduced with v_dot2 against the row's weight pairs,
+//      and the eight slot groups' partial scores meet in an 8-lane DPP sum;
+//   2. BCE loss and dlogit g: lane u computes sample 4q + (u & 3) and the
+//      quad's four values reach every lane of it by DPP broadcast;
+//   3. dW: two v_dot2 per slot over the lane's four samples (g rounded to
+//      bf16), then a reduce-scatter over the four quads: one
+//      v_permlane16_swap level and one DPP level (register i holds slot
+//      i ^ 2(q & 1) of the group; the lane keeps slots 2q, 2q+1);
 //   4. Adam on those two slots, streaming W, m, v back to HBM;
 //   5. dX: g and the old weights go to G and T, and the matrix cores add
 //      G x T^T (16 x 16 by 16 x d) into a per-workgroup dX in registers (each
@@ -142,14 +145,12 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
 
     const int tid = threadIdx.x;
     const int lab = tid >> 5, u = tid & 31;
-    const int h = u >> 4, bs = u & 15;          // slot half, sample of the pass
+    const int qd = u >> 3, grp = u & 7;         // sample quad of the pass, slot group of the row
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-    // register r of the lane holds slot r ^ Kp of its half; the reduce-scatter
-    // leaves it with slots Kown, Kown + 1 of the half
-    const int Kp = lane_key(bs) & ~2;
-    const int Kown = Kp + 2 * (bs & 1);
-    const int myslot = 32 * h + Kown;
-    const bool odd = (bs & 1) != 0;
+    // the reduce-scatter over the quads leaves the lane with slots 2 qd,
+    // 2 qd + 1 of its group
+    const int myslot = 8 * grp + 2 * qd;
+    const int sj = grp & 3;                     // the sample of its quad whose dlogit the lane computes
     const int nnz = a.nnz;
     const bool tg_lds = nnz <= WD_TG_MAX;
     uint32_t *ymw = tg + 2 * wave;   // scan path: this wave's two rows' masks
@@ -282,10 +283,10 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
             yrow = ymw[lab & 1];
         }
         int rl = lab;            // the row of the chunk this lane serves
-        int k4 = Kp >> 2;        // quad order of this lane
+        int kq = qd & 1;         // pair order of this lane's registers
         // opaque per chunk, so the per-slot LDS addresses are formed where
         // they are used instead of being held in registers across chunks
-        asm volatile("" : "+v"(rl), "+v"(k4));
+        asm volatile("" : "+v"(rl), "+v"(kq));
         const int64_t l = l0 + rl;
         const bool valid = l < a.L;
         const uint32_t obm = valid && u == 0 ? (uint32_t)l * 4u : a.nb_b;
@@ -302,72 +303,89 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
             dbprev = ldf(R.dbp, obm);
         }
 
-        // gather the lane's 32 slots as bf16 pairs (register p <-> slots
-        // 2p ^ Kp, (2p ^ Kp) + 1 of the half) and run the forward on the fly
-        uint32_t xp[16];
-        int32_t c0n = 0, c1n = 0;
-        uint32_t wown = 0u;
-        float za = 0.f, zb = 0.f;
-        const int32_t *Ish = Is + rl * WD_K + 32 * h;
-        const uint32_t *Wsh = reinterpret_cast<const uint32_t *>(Ws) + rl * (WD_K / 2) + 16 * h;
+        // gather the lane's 8 slots for its 4 samples: registers 2p, 2p+1
+        // hold slots 2(p ^ kq), 2(p ^ kq) + 1 of the group, each as the
+        // samples' bf16 pairs (4q, 4q+1 | 4q+2, 4q+3)
+        const int32_t *Ig = Is + rl * WD_K + 8 * grp;
+        const uint4 wq = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint32_t *>(Ws) +
+                                                          rl * (WD_K / 2) + 4 * grp);
+        const unsigned char *Xq = Xs + 8 * qd;
+        uint2 xv[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int qq = q ^ k4;   // pairs 2q, 2q+1 hold slots 4qq..4qq+3 of the half
-            const int4 iv = *reinterpret_cast<const int4 *>(Ish + 4 * qq);
-            const uint2 wv = *reinterpret_cast<const uint2 *>(Wsh + 2 * qq);
-            if (q == 0) {   // the lane's own slots are the first pair (odd: the second)
-                c0n = (odd ? iv.z : iv.x) / WD_XS;
-                c1n = (odd ? iv.w : iv.y) / WD_XS;
-                wown = odd ? wv.y : wv.x;
-            }
-            bf16x2 p0, p1;
-            p0[0] = *reinterpret_cast<const __bf16 *>(Xs + iv.x + 2 * bs);
-            p0[1] = *reinterpret_cast<const __bf16 *>(Xs + iv.y + 2 * bs);
-            p1[0] = *reinterpret_cast<const __bf16 *>(Xs + iv.z + 2 * bs);
-            p1[1] = *reinterpret_cast<const __bf16 *>(Xs + iv.w + 2 * bs);
-            xp[2 * q] = __builtin_bit_cast(uint32_t, p0);
-            xp[2 * q + 1] = __builtin_bit_cast(uint32_t, p1);
-            za = dot2(xp[2 * q], wv.x, za);
-            zb = dot2(xp[2 * q + 1], wv.y, zb);
+        for (int p = 0; p < 4; ++p) {
+            const int2 io = *reinterpret_cast<const int2 *>(Ig + 2 * (p ^ kq));
+            xv[2 * p] = *reinterpret_cast<const uint2 *>(Xq + io.x);
+            xv[2 * p + 1] = *reinterpret_cast<const uint2 *>(Xq + io.y);
         }
-        // the two halves of the row add up their partial sums
-        const float zz = cross_rows_add(za + zb, za + zb) + cur.b;
-        // BCE and dlogit of (row, sample); zero for padded samples and rows
-        // past L; the loss is counted once, in half 0
-        const bool live = valid && bs < a.B;
-        const float y = ((yrow >> bs) & 1u) ? 1.f : 0.f;
-        float g;
+        // the lane's own slots 2 qd, 2 qd + 1: their columns and weight pair
+        const int2 co = *reinterpret_cast<const int2 *>(Ig + 2 * qd);
+        const int32_t c0n = co.x / WD_XS, c1n = co.y / WD_XS;
+        const uint32_t wown = qd == 0 ? wq.x : qd == 1 ? wq.y : qd == 2 ? wq.z : wq.w;
+        // forward: the weight pairs in register order
+        const uint32_t wp[4] = {kq ? wq.y : wq.x, kq ? wq.x : wq.y, kq ? wq.w : wq.z, kq ? wq.z : wq.w};
+        float z[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const uint2 A = xv[2 * p], Bv = xv[2 * p + 1];
+            z[0] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x05040100u), wp[p], z[0]);
+            z[1] = dot2(__builtin_amdgcn_perm(Bv.x, A.x, 0x07060302u), wp[p], z[1]);
+            z[2] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x05040100u), wp[p], z[2]);
+            z[3] = dot2(__builtin_amdgcn_perm(Bv.y, A.y, 0x07060302u), wp[p], z[3]);
+        }
+        // the eight slot groups (lanes of one half DPP row) add up their scores
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float t = add_dpp<DPP_ROW_HALF_MIRROR>(z[e], z[e]);
+            t = add_dpp<DPP_QUAD_3210>(t, t);
+            z[e] = add_dpp<DPP_QUAD_1032>(t, t);
+        }
+        // BCE and dlogit of (row, sample 4 qd + sj); zero for padded samples
+        // and rows past L; the loss is counted once, by the lanes with g < 4
+        const int bj = 4 * qd + sj;
+        const float zz = (sj == 0 ? z[0] : sj == 1 ? z[1] : sj == 2 ? z[2] : z[3]) + cur.b;
+        const bool live = valid && bj < a.B;
+        const float y = ((yrow >> bj) & 1u) ? 1.f : 0.f;
+        float gj;
         if (a.hinge) {
             // squared hinge with yh = 2y - 1
             const float yh = 2.f * y - 1.f;
             const float hh = fmaxf(1.f - yh * zz, 0.f);
-            loss_acc += live && h == 0 ? hh * hh : 0.f;
-            g = live ? -2.f * a.s * yh * hh : 0.f;
+            loss_acc += live && grp < 4 ? hh * hh : 0.f;
+            gj = live ? -2.f * a.s * yh * hh : 0.f;
         } else {
             const float ex = __builtin_amdgcn_exp2f(-fabsf(zz) * 1.4426950408889634f);
             const float opx = 1.f + ex;
             const float rr = __builtin_amdgcn_rcpf(opx);
             const float sig = zz >= 0.f ? rr : ex * rr;
-            loss_acc += live && h == 0 ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
-                                       : 0.f;
-            g = live ? a.s * (sig - y) : 0.f;
+            loss_acc += live && grp < 4
+                            ? fmaxf(zz, 0.f) - zz * y + __builtin_amdgcn_logf(opx) * 0.6931471805599453f
+                            : 0.f;
+            gj = live ? a.s * (sig - y) : 0.f;
         }
-        // dW partials of the lane's slots, slot order r ^ Kp
-        const uint32_t glo = pack_bf16(g, 0.f), ghi = pack_bf16(0.f, g);
+        // every lane of a quad gets the dlogits of its four samples (lane i of
+        // each group of four computed sample 4 qd + i)
+        const int gji = __float_as_int(gj);
+        const float g[4] = {__int_as_float(__builtin_amdgcn_update_dpp(0, gji, 0x00, 0xf, 0xf, false)),
+                            __int_as_float(__builtin_amdgcn_update_dpp(0, gji, 0x55, 0xf, 0xf, false)),
+                            __int_as_float(__builtin_amdgcn_update_dpp(0, gji, 0xAA, 0xf, 0xf, false)),
+                            __int_as_float(__builtin_amdgcn_update_dpp(0, gji, 0xFF, 0xf, 0xf, false))};
+        // dW partials of the lane's slots over its samples, register order
+        const uint32_t g01 = pack_bf16(g[0], g[1]), g23 = pack_bf16(g[2], g[3]);
         // a wave whose dlogits are all zero (a hinge loss past its margin
         // everywhere, Sec. 2.2) has zero dW: its products are skipped
         float dw0 = dprev.x, dw1 = dprev.y;
-        if (__builtin_amdgcn_ballot_w64(glo != 0u) != 0) {
-            float pw[32];
+        if (__builtin_amdgcn_ballot_w64((g01 | g23) != 0u) != 0) {
+            float pw[8];
 #pragma unroll
-            for (int p = 0; p < 16; ++p) {
-                pw[2 * p] = dot2z(xp[p], glo);
-                pw[2 * p + 1] = dot2z(xp[p], ghi);
-            }
-            // reduce-scatter over the pass's 16 samples
-            const float2 dws = reduce_scatter16(pw, odd);
-            dw0 += dws.x;
-            dw1 += dws.y;
+            for (int i = 0; i < 8; ++i) pw[i] = dot2(xv[i].y, g23, dot2z(xv[i].x, g01));
+            // reduce-scatter over the four quads: quads qd and qd ^ 2 sit in
+            // the two DPP rows of the row's 32 lanes, quads qd and qd ^ 1 8
+            // lanes apart in one DPP row
+            float r4[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) r4[t] = cross_rows_add(pw[t], pw[4 + t]);
+            dw0 += add_dpp<DPP_ROW_ROR8>(r4[0], r4[2]);
+            dw1 += add_dpp<DPP_ROW_ROR8>(r4[1], r4[3]);
         }
         if constexpr (!ADAM) stf2(R.dwp, odw, make_float2(dw0, dw1));
         if constexpr (ADAM) {
@@ -381,10 +399,12 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
             stf2(R.v, valid ? 4u * o : a.nb_m, make_float2(v0, v1));
             st32(R.W, valid ? 2u * o : a.nb_W, pack_bf16(n0, n1));
         }
-        // bias: sum of g over the pass's samples (half 0's lanes), lane u == 0
-        // updates
+        // bias: sum of g over the pass's samples (the quad's four, then the
+        // four quads), lane u == 0 updates
         {
-            const float sg = sum16(g) + dbprev;
+            float sg = (g[0] + g[1]) + (g[2] + g[3]);
+            sg = cross_rows_add(sg, sg);
+            sg = add_dpp<DPP_ROW_ROR8>(sg, sg) + dbprev;
             if constexpr (ADAM) {
                 float mm = bmcur, vv = bvcur;
                 const float nb = adam_step(cur.b, sg, mm, vv, b1, b2, inv_bc1, inv_bc2, lr, eps, decay);
@@ -403,7 +423,7 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
         T[qswz(c0, kk)] = 0;
         T[qswz(c1, kk)] = 0;
         // dX inputs: g and the old weights (a row past L writes zeros at column 0)
-        if (h == 0) G[qswz(bs, kk)] = (uint16_t)(glo & 0xffffu);
+        if (grp < 4) G[qswz(bj, kk)] = (uint16_t)(pack_bf16(gj, 0.f) & 0xffffu);
         T[qswz(c0n, kk)] = (uint16_t)(wown & 0xffffu);
         T[qswz(c1n, kk)] = (uint16_t)(wown >> 16);
         c0 = c0n;
