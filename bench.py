@@ -315,6 +315,8 @@ def main():
     ap.add_argument("--hinge-reps", type=int, default=10,
                     help="squared hinge steps per case (0 skips them, e.g. under a kernel trace "
                          "whose per-kernel average should cover the BCE step only)")
+    ap.add_argument("--copy-reps", type=int, default=5,
+                    help="timed 1 GiB device copies for the achievable streaming rate (0 skips them)")
     ap.add_argument("--composed-reps", type=int, default=5,
                     help="whole steps of the workloads with dense parts, each (0 skips them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -410,6 +412,10 @@ def main():
     print("[bench] timed %d steps: %.3f ms/step, sweep kernel %.3f ms avg, loss %.5f" %
           (args.steps, ms_per_step, kern_avg_ms, final_loss), file=sys.stderr, flush=True)
 
+    # device memory held for the step: the layer state, its workspace and the
+    # batch (torch's peak counter; the paper's memory metric)
+    peak_mem = int(torch.cuda.max_memory_allocated())
+    state_bytes = ffsl.footprint_bytes(w.L, w.k, vb, bias=True)
     step_bytes = fused_step_bytes(w, vb)
     achieved = step_bytes / (kern_avg_ms * 1e-3) / 1e9
     src_hash = sweep_source_hash()
@@ -545,6 +551,27 @@ def main():
     print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
           (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
 
+    # the achievable streaming rate on this device: a plain 1 GiB device copy
+    # (read + write), median of a few, event-timed
+    copy = None
+    if args.copy_reps > 0:
+        nb = 1 << 30
+        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        cms = []
+        for _ in range(args.copy_reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dst.copy_(src)
+            b.record()
+            torch.cuda.synchronize()
+            cms.append(a.elapsed_time(b))
+        del src, dst
+        cmed = sorted(cms)[len(cms) // 2]
+        copy = {"bytes": 2 * nb, "ms_median": cmed, "gbs": 2 * nb / (cmed * 1e-3) / 1e9}
+        print("[bench] device copy: %.0f GB/s (read + write)" % copy["gbs"], file=sys.stderr, flush=True)
+
     composed = None
     if args.composed_reps > 0:
         composed = time_composed(torch, ffsl, synth, ev, stream, dev, args.composed_reps, args.seed)
@@ -584,7 +611,11 @@ def main():
             "algorithmic_bytes_per_launch": step_bytes,
             "kernel_ms_avg": kern_avg_ms,
             "source_hash": src_hash,
+            "frac_of_copy": achieved / copy["gbs"] if copy else None,
         },
+        "copy_peak": copy,
+        "memory": {"peak_allocated_bytes": peak_mem, "layer_state_bytes": state_bytes,
+                   "note": "torch.cuda.max_memory_allocated after the timed steps (state, workspace, batch)"},
         "set_update": {
             "ms_median": set_ms_med,
             "algorithmic_bytes": sb,
@@ -592,6 +623,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": set_gbs / HBM_PEAK_GBS,
+            "frac_of_copy": set_gbs / copy["gbs"] if copy else None,
             "prune_per_row": n_set,
         },
         "set_in_step": {
