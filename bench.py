@@ -610,6 +610,8 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": step_bytes,
             "kernel_ms_avg": kern_avg_ms,
+            "kernel_ms_median": sorted(kern_ms)[len(kern_ms) // 2],
+            "kernel_ms_min": min(kern_ms),
             "source_hash": src_hash,
             "frac_of_copy": achieved / copy["gbs"] if copy else None,
         },
