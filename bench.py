@@ -243,6 +243,53 @@ def time_composed(torch, ffsl, synth, ev, stream, dev, reps, seed):
     return out
 
 
+def time_c2_run(torch, ffsl, synth, dev, seed):
+    """The C2 workload's whole run: 100 fused training steps on fresh seeded
+    batches (all uploaded before the timed region), SET fused into the step
+    after every 20th (ffsl_train_step_set), timed with torch events around
+    the run."""
+    import numpy as np
+    w = synth.WORKLOADS["c2_bf16_L131072"]
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    inp = synth.make_layer_inputs(w, seed)
+    host = synth.make_batches(w, w.steps, seed)
+    batches = [(bf(X), torch.from_numpy(off.astype(np.int32)).to(dev), torch.from_numpy(lab).to(dev))
+               for X, off, lab in host]
+    nnz_max = max(len(b[2]) for b in host)
+    layer = ffsl.SparseLayer(bf(inp.W), torch.from_numpy(inp.I).to(dev), bias=torch.from_numpy(inp.bias).to(dev),
+                             B_max=w.B, nnz_max=nnz_max, unfused=False).bind(w.d)
+    loss = torch.empty(1, device=dev)
+    dX = torch.empty((w.B, w.d), device=dev)
+    ex = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def run():
+        for t in range(1, w.steps + 1):
+            X, off, lab = batches[t - 1]
+            if t % w.set_every == 0:
+                layer.train_step_set(X, off, lab, t, w.set_frac, seed, t // w.set_every, loss_out=loss, dX_out=dX,
+                                     mask=False, exhausted_out=ex)
+            else:
+                layer.train_step(X, off, lab, t, loss_out=loss, dX_out=dX)
+
+    run()   # a first run warms up; the timed run continues from its state
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b)
+    out = {"steps": w.steps, "set_every": w.set_every, "set_frac": w.set_frac, "ms_total": ms,
+           "ms_per_step": ms / w.steps, "value": w.B * w.L * w.steps / (ms * 1e-3), "unit": "sample*labels/s",
+           "exhausted_rows": int(ex.cpu()[0]),
+           "shape": {"L": w.L, "k": w.k, "B": w.B, "d": w.d}}
+    layer.close()
+    return out
+
+
 def cpu_baseline(w, inp, target_s=12.0):
     """The oracle (float64, single thread) on the first L' label rows of the
     same workload: one fused step (forward, BCE, backward, Adam)."""
@@ -317,6 +364,8 @@ def main():
                          "whose per-kernel average should cover the BCE step only)")
     ap.add_argument("--copy-reps", type=int, default=5,
                     help="timed 1 GiB device copies for the achievable streaming rate (0 skips them)")
+    ap.add_argument("--c2-run", type=int, default=1,
+                    help="time the C2 workload's 100-step run with SET every 20 steps (0 skips it)")
     ap.add_argument("--composed-reps", type=int, default=5,
                     help="whole steps of the workloads with dense parts, each (0 skips them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -572,6 +621,13 @@ def main():
         copy = {"bytes": 2 * nb, "ms_median": cmed, "gbs": 2 * nb / (cmed * 1e-3) / 1e9}
         print("[bench] device copy: %.0f GB/s (read + write)" % copy["gbs"], file=sys.stderr, flush=True)
 
+    c2_run = None
+    if args.c2_run:
+        c2_run = time_c2_run(torch, ffsl, synth, dev, args.seed)
+        print("[bench] C2 run: %d steps with SET every %d in %.2f ms (%.3f ms/step)" %
+              (c2_run["steps"], c2_run["set_every"], c2_run["ms_total"], c2_run["ms_per_step"]),
+              file=sys.stderr, flush=True)
+
     composed = None
     if args.composed_reps > 0:
         composed = time_composed(torch, ffsl, synth, ev, stream, dev, args.composed_reps, args.seed)
@@ -645,6 +701,7 @@ def main():
         "dense_gelu": dense["dense_gelu"],
         "aux_head": dense["aux_head"],
         "composed_step": composed,
+        "c2_run": c2_run,
         "cpu_baseline": cpu,
         "loss": final_loss,
     }
