@@ -131,6 +131,49 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Ascending sort of a 512-thread workgroup's keys into tg (room for 1024
+// words).  Thread t brings the keys of elements t and t + 512 (k0, k1; empty
+// elements hold 0xffffffff), n of them in all, n <= 1024.  A bitonic network
+// over N = max(64, next power of two >= n) elements: a stage whose partners
+// lie within a wave (distance < 64) exchanges registers through a lane
+// shuffle, with no barrier; the few stages across waves go through tg between
+// two barriers; the one stage at distance 512 (N = 1024) swaps a thread's own
+// pair.  On return tg[0 .. N) holds the keys in ascending order, visible to
+// the whole workgroup.
+__device__ __forceinline__ uint32_t bitonic_pick(uint32_t x, uint32_t y, int i, int j, int k) {
+    return (((i & j) == 0) == ((i & k) == 0)) ? min(x, y) : max(x, y);
+}
+__device__ __forceinline__ void sort_keys512(uint32_t *tg, uint32_t k0, uint32_t k1, int n, int tid) {
+    int N = 64;
+    while (N < n) N <<= 1;
+    const bool two = N > 512;
+    const bool own = tid < N;   // whole waves: N is a multiple of 64
+    for (int k = 2; k <= N; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= 512) {
+                // N = 1024, k = 1024: element tid is the lower of its own pair
+                const uint32_t lo = min(k0, k1), hi = max(k0, k1);
+                k0 = lo;
+                k1 = hi;
+            } else if (j >= 64) {
+                __syncthreads();   // the previous exchange's reads are done
+                if (own) tg[tid] = k0;
+                if (two) tg[tid + 512] = k1;
+                __syncthreads();
+                if (own) k0 = bitonic_pick(k0, tg[tid ^ j], tid, j, k);
+                if (two) k1 = bitonic_pick(k1, tg[(tid + 512) ^ j], tid + 512, j, k);
+            } else {
+                if (own) k0 = bitonic_pick(k0, (uint32_t)__shfl_xor((int)k0, j), tid, j, k);
+                if (two) k1 = bitonic_pick(k1, (uint32_t)__shfl_xor((int)k1, j), tid + 512, j, k);
+            }
+        }
+    }
+    __syncthreads();
+    if (own) tg[tid] = k0;
+    if (two) tg[tid + 512] = k1;
+    __syncthreads();
+}
+
 // Adam with the bias corrections folded into reciprocals; fp32 throughout
 __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &vv, float b1, float b2,
                                            float inv_bc1, float inv_bc2, float lr, float eps, float decay) {

@@ -218,37 +218,20 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         for (int e = tid; e < d * MX_NLAB / 2; e += MX_THREADS) reinterpret_cast<uint32_t *>(T)[e] = 0u;
     }
     // The batch's positives as keys (label << 6 | sample), sorted ascending
-    // (bitonic sort in LDS; a label outside [0,L) becomes the largest key and
+    // (sort_keys512: a bitonic network, lane shuffles within waves and LDS across
+    // them; a label outside [0,L) becomes the largest key and
     // is never matched).  Chunks of one workgroup come in ascending order, so
     // a cursor that only moves forward finds each chunk's positives.
     if (tg_lds) {
-        int n2 = 1;
-        while (n2 < nnz) n2 <<= 1;
-        for (int e = tid; e < n2; e += MX_THREADS) {
-            uint32_t key = 0xffffffffu;
-            if (e < nnz) {
-                const int32_t lb = a.tgt_lab[e];
-                const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
-                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B) key = ((uint32_t)lb << 6) | (uint32_t)sb;
-            }
-            tg[e] = key;
-        }
-        __syncthreads();
-        for (int k = 2; k <= n2; k <<= 1) {
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                for (int i = tid; i < n2; i += MX_THREADS) {
-                    const int ij = i ^ j;
-                    if (ij > i) {
-                        const uint32_t x = tg[i], y = tg[ij];
-                        if (((i & k) == 0) ? (x > y) : (x < y)) {
-                            tg[i] = y;
-                            tg[ij] = x;
-                        }
-                    }
-                }
-                __syncthreads();
-            }
-        }
+        auto key_of = [&](int e) -> uint32_t {
+            if (e >= nnz) return 0xffffffffu;
+            const int32_t lb = a.tgt_lab[e];
+            const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
+            return lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B ? ((uint32_t)lb << 6) | (uint32_t)sb
+                                                                       : 0xffffffffu;
+        };
+        static_assert(MX_THREADS == 512, "sort_keys512 takes a 512-thread workgroup");
+        sort_keys512(tg, key_of(tid), key_of(tid + MX_THREADS), nnz, tid);
     }
 
     // dX accumulators: 4 batch tiles x NT column tiles of 16 per wave (8 waves)

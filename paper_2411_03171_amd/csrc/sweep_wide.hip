@@ -189,37 +189,20 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
         for (int e = tid; e < (d * WD_NLAB + WD_NB * WD_NLAB) / 2; e += WD_THREADS) TG[e] = 0u;
     }
     // The pass's positives as keys (label << 4 | sample), sorted ascending
-    // (bitonic sort in LDS; a label outside [0,L) becomes the largest key and
+    // (sort_keys512: a bitonic network, lane shuffles within waves and LDS across
+    // them; a label outside [0,L) becomes the largest key and
     // is never matched).  Chunks of one workgroup come in ascending order, so
     // a cursor that only moves forward finds each chunk's positives.
     if (tg_lds) {
-        int n2 = 1;
-        while (n2 < nnz) n2 <<= 1;
-        for (int e = tid; e < n2; e += WD_THREADS) {
-            uint32_t key = 0xffffffffu;
-            if (e < nnz) {
-                const int32_t lb = a.tgt_lab[e];
-                const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
-                if (lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B) key = ((uint32_t)lb << 4) | (uint32_t)sb;
-            }
-            tg[e] = key;
-        }
-        __syncthreads();
-        for (int k = 2; k <= n2; k <<= 1) {
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                for (int i = tid; i < n2; i += WD_THREADS) {
-                    const int ij = i ^ j;
-                    if (ij > i) {
-                        const uint32_t x = tg[i], y = tg[ij];
-                        if (((i & k) == 0) ? (x > y) : (x < y)) {
-                            tg[i] = y;
-                            tg[ij] = x;
-                        }
-                    }
-                }
-                __syncthreads();
-            }
-        }
+        auto key_of = [&](int e) -> uint32_t {
+            if (e >= nnz) return 0xffffffffu;
+            const int32_t lb = a.tgt_lab[e];
+            const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
+            return lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B ? ((uint32_t)lb << 4) | (uint32_t)sb
+                                                                       : 0xffffffffu;
+        };
+        static_assert(WD_THREADS == 512, "sort_keys512 takes a 512-thread workgroup");
+        sort_keys512(tg, key_of(tid), key_of(tid + WD_THREADS), nnz, tid);
     }
     __syncthreads();
 
