@@ -1,5 +1,6 @@
-"""SET at the full size of the largest workload (L = 3 145 728 labels, k = 32,
-d = 768, bf16): both prune modes against the oracle on three blocks of rows
+"""SET at full size: the largest workload (L = 3 145 728 labels, k = 32,
+d = 768, bf16) and the C3 sparse layer (L = 1 048 576, k = 64, d = 2048).
+The largest workload: both prune modes against the oracle on three blocks of rows
 (start, middle, end; the draw counter of a row is its index in the layer, so
 a block is checked with the oracle's row offset), and the training step with
 SET in one call against the step followed by SET, bit for bit over the whole
@@ -92,3 +93,38 @@ def test_fused_step_set_full_c4_equals_step_then_set(c4_inputs):
                        ("loss", la.view(torch.int32), lb.view(torch.int32)), ("exhausted", exa, exb)):
         assert torch.equal(x, y), name
     assert int(ma.sum().item()) == w.L * int(np.floor(w.set_frac * w.k + 1e-9))
+
+
+def test_set_full_c3_against_oracle():
+    """SET on the full C3 sparse layer (L = 1 048 576, k = 64, d = 2048: rows too
+    wide for the LDS tiles, so the one-lane-per-row kernel), fraction mode, on
+    three row blocks against the oracle."""
+    import torch
+    w = synth.dataclasses.replace(synth.WORKLOADS["c3_inter2048_L1M"], din=0)
+    note("full-size SET c3: generating inputs")
+    inp = synth.make_layer_inputs(w, 1)
+    seed, rnd = 0xC3C3C3C3, 5
+    note("full-size SET c3: GPU")
+    layer = _layer(inp, w)
+    mask, ex = layer.set_update(w.set_frac, seed, rnd)
+    torch.cuda.synchronize()
+    assert int(ex.cpu()[0]) == 0
+    starts = [0, w.L // 2 - ROWS // 2, w.L - ROWS]
+    got = []
+    for r0 in starts:
+        sl = slice(r0, r0 + ROWS)
+        got.append((from_torch_bits(layer.W[sl], "bf16"), layer.I[sl].cpu().numpy(), layer.m[sl].cpu().numpy(),
+                    mask[sl].cpu().numpy()))
+    del layer
+    torch.cuda.empty_cache()
+    zeros = np.zeros((ROWS, w.k), dtype=np.float32)
+    for r0, (Wg, Ig, mg, maskg) in zip(starts, got):
+        note("full-size SET c3: oracle rows %d.." % r0)
+        sl = slice(r0, r0 + ROWS)
+        Wr, Ir, mr, vr, maskr, exr = oracle.set_update(inp.W[sl], inp.I[sl], zeros, zeros, w.d, w.set_frac,
+                                                       seed, rnd, row0=r0)
+        assert exr == 0
+        np.testing.assert_array_equal(Ig, Ir)
+        np.testing.assert_array_equal(maskg, maskr)
+        np.testing.assert_array_equal(Wg, Wr)
+        np.testing.assert_array_equal(mg.view(np.uint32), mr.view(np.uint32))
