@@ -25,6 +25,10 @@
  *   philox4x64_10        numpy.random.Philox (a library implementation)
  *   set_update           stable argsort, brute force, invariants; the draw
  *                        stream itself is our own contract (see set_update)
+ *   set_update_threshold a plain-Python restatement; reduces to the fraction
+ *                        mode when tau selects exactly n slots; extremes
+ *   topk, precision_at_k numpy lexsort on tied / NaN / -inf scores, a
+ *                        set-based P@k count, a hand-computed case
  *   gelu / dense / aux   closed forms + torch autograd
  */
 #include <math.h>
