@@ -63,6 +63,11 @@ WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_m
     if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L * (size_t)k);
     w.dbp = off;
     if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L);
+    w.has_xt = wide || (k == 32 && d % 128 == 0 && d >= 128 && d <= 768);
+    w.keys = off;
+    if (w.has_xt) off = align256(off + sizeof(uint32_t) * 1024 * (size_t)passes);
+    w.xt = off;
+    if (w.has_xt) off = align256(off + sizeof(uint16_t) * (size_t)passes * pass_b * (size_t)d);
     w.total = off;
     return w;
 }

@@ -33,7 +33,10 @@ struct WsLayout {
     size_t dx_part;     // float [max_parts][B_max][d]
     size_t dwp, dbp;    // float [L][k], [L]: dW / dbias carried between the
                         // batch passes of the fused fast path (B_max > 64, k = 32)
+    size_t keys;        // uint32 [passes][1024]: each pass's sorted positives
+    size_t xt;          // bf16 [passes][d][pass width]: the batch transposed per pass
     bool has_partial;
+    bool has_xt;        // the shape may take a fused fast path (keys, xt allocated)
     size_t total;
 };
 WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts);
@@ -115,12 +118,21 @@ struct SweepCall {
 };
 
 int launch_sweep(const SweepCall &c);
+// the fused fast paths' per-call batch preparation: sorted positives per pass
+// (when nnz <= 1024) and the batch transposed per pass (batch_prep.hip)
+int launch_batch_prep(const uint16_t *X, int32_t B, int32_t d, const int32_t *off, const int32_t *lab,
+                      int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, hipStream_t st);
+// what the fast sweeps read besides the layer and the call
+struct FastBufs {
+    const int32_t *tgt_b;     // sample of each positive (used when nnz > 1024)
+    const uint32_t *keys;     // [passes][1024] sorted positives (nnz <= 1024)
+    const uint16_t *xt;       // [passes][d][pass width] transposed batch
+    float *loss_part, *dx_part, *dwp, *dbp;
+};
 bool sweep_mx_eligible(const Layer &ly, int B, int mode);
-int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
-                    float *dbp, int *grid_out, int *passes_out);
+int launch_sweep_mx(const SweepCall &c, const FastBufs &fb, int *grid_out, int *passes_out);
 bool sweep_wide_eligible(const Layer &ly, int mode);
-int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
-                      float *dbp, int *grid_out, int *passes_out);
+int launch_sweep_wide(const SweepCall &c, const FastBufs &fb, int *grid_out, int *passes_out);
 int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 // SET; in threshold mode (tau >= 0) every slot with |W| < tau is pruned and n
 // is ignored

@@ -457,27 +457,36 @@ int launch_sweep(const SweepCall &c) {
 
     int grid = (int)std::min<int64_t>(a.nchunks, ly.max_parts);
 
-    if (c.nnz > 0) {
+    // the fused fast paths
+    const bool use_wide = wl.has_xt && sweep_wide_eligible(ly, c.mode) && (B <= WD_PASS_B || wl.has_partial);
+    const bool use_mx =
+        !use_wide && wl.has_xt && sweep_mx_eligible(ly, B, c.mode) && (B <= MX_PASS_B || wl.has_partial);
+    const bool fast = use_wide || use_mx;
+
+    // the sample of every positive: the general path, and the fast paths when
+    // the positives are too many for their sorted list in LDS
+    if (c.nnz > 0 && (!fast || c.nnz > 1024)) {
         hipLaunchKernelGGL(k_targets_prep, dim3((B + 255) / 256), dim3(256), 0, c.stream, c.tgt_off, B,
                            c.nnz, const_cast<int32_t *>(a.tgt_b));
         int rc = check_launch("targets_prep");
         if (rc) return rc;
     }
 
-    // the fast paths read X in 16-byte rows
-    if (sweep_wide_eligible(ly, c.mode) && (B <= WD_PASS_B || wl.has_partial) &&
-        (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
-        int passes = 1;
-        int rc = launch_sweep_wide(c, a.tgt_b, a.loss_part, a.dx_part, reinterpret_cast<float *>(ly.ws + wl.dwp),
-                                   reinterpret_cast<float *>(ly.ws + wl.dbp), &grid, &passes);
+    if (fast) {
+        FastBufs fb{};
+        fb.tgt_b = a.tgt_b;
+        fb.keys = reinterpret_cast<const uint32_t *>(ly.ws + wl.keys);
+        fb.xt = reinterpret_cast<const uint16_t *>(ly.ws + wl.xt);
+        fb.loss_part = a.loss_part;
+        fb.dx_part = a.dx_part;
+        fb.dwp = reinterpret_cast<float *>(ly.ws + wl.dwp);
+        fb.dbp = reinterpret_cast<float *>(ly.ws + wl.dbp);
+        int rc = launch_batch_prep(static_cast<const uint16_t *>(c.X), B, d, c.tgt_off, c.tgt_lab, c.nnz, ly.L,
+                                   use_wide ? WD_PASS_B : MX_PASS_B, reinterpret_cast<uint32_t *>(ly.ws + wl.keys),
+                                   reinterpret_cast<uint16_t *>(ly.ws + wl.xt), c.stream);
         if (rc) return rc;
-        return finish_sweep(c, a.loss_part, a.dx_part, grid * passes, B, d, grid);
-    }
-    if (sweep_mx_eligible(ly, B, c.mode) && (B <= MX_PASS_B || wl.has_partial) &&
-        (reinterpret_cast<uintptr_t>(c.X) & 15u) == 0) {
         int passes = 1;
-        int rc = launch_sweep_mx(c, a.tgt_b, a.loss_part, a.dx_part, reinterpret_cast<float *>(ly.ws + wl.dwp),
-                                 reinterpret_cast<float *>(ly.ws + wl.dbp), &grid, &passes);
+        rc = use_wide ? launch_sweep_wide(c, fb, &grid, &passes) : launch_sweep_mx(c, fb, &grid, &passes);
         if (rc) return rc;
         return finish_sweep(c, a.loss_part, a.dx_part, grid * passes, B, d, grid);
     }

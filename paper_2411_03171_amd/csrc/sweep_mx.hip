@@ -63,7 +63,8 @@ struct MxArgs {
     int64_t L;
     int32_t d, B, nnz;
     int64_t nchunks;
-    const uint16_t *X;
+    const uint16_t *XT;     // this pass's samples transposed, [d][64] (batch prep)
+    const uint32_t *keys;   // this pass's sorted positives, [1024] (nnz <= 1024)
     uint16_t *W;
     const int32_t *I;
     float *bias, *m, *v, *bm, *bv;
@@ -74,7 +75,7 @@ struct MxArgs {
     float *dx_part;
     // array sizes in bytes: the range of each buffer resource, and the offset
     // that the chunk loop uses for an access that must not happen
-    uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    uint32_t nb_W, nb_I, nb_m, nb_b;
     int32_t idx16;   // I holds uint16 indices
     // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
     // passes in dwp [L][32], dbp [L]
@@ -93,7 +94,7 @@ struct MxArgs {
 constexpr int MX_ONLY = PASS_ONLY, MX_FIRST = PASS_FIRST, MX_LAST = PASS_LAST, MX_MIDDLE = PASS_MIDDLE;
 
 struct Rsrcs {
-    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp, mk;
+    Rsrc XT, K, W, I, m, v, b, bm, bv, dwp, dbp, mk;
 };
 
 constexpr int MX_SET_NMAX = 8;   // pruned slots per row the fused SET handles
@@ -183,7 +184,8 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     const bool tg_lds = nnz <= MX_TG_MAX;
 
     Rsrcs R;
-    R.X = make_rsrc(a.X, a.nb_X);
+    R.XT = make_rsrc(a.XT, (uint32_t)d * MX_XS);
+    R.K = make_rsrc(a.keys, tg_lds ? MX_TG_MAX * 4u : 0u);
     R.W = make_rsrc(a.W, a.nb_W);
     R.I = make_rsrc(a.I, a.nb_I);
     R.m = make_rsrc(a.m, a.nb_m);
@@ -198,41 +200,26 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
     Prefetch pa, pb;
     prefetch<ADAM>(a, R, blockIdx.x, tid, lab, u, Kown, pa);
 
-    // stage X transposed (b fastest) and zero past B; clear T
+    // stage the pass's X tile (transposed and zero-padded past B by the batch
+    // prep) with 16-byte copies, its sorted positives, and clear T.  The
+    // positives are keys (label << 6 | sample), ascending (a label outside
+    // [0,L) is the largest key and is never matched).  Chunks of one
+    // workgroup come in ascending order, so a cursor that only moves forward
+    // finds each chunk's positives.
     {
-        // lane = sample, each wave takes groups of 8 columns: 16-byte row loads,
-        // conflict-free 2-byte LDS stores
-        uint16_t *X16 = reinterpret_cast<uint16_t *>(Xs);
-        const int b = lane;
-#pragma unroll 6
-        for (int gi = wave; gi < d / 8; gi += MX_THREADS / 64) {
-            const uint32_t ox = b < a.B ? (uint32_t)((a.b0 + b) * d + 8 * gi) * 2u : a.nb_X;
-            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.X, ox, 0, 0);
-            const uint32_t w4[4] = {q[0], q[1], q[2], q[3]};
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                X16[(8 * gi + 2 * j) * MX_NB + b] = (uint16_t)(w4[j] & 0xffffu);
-                X16[(8 * gi + 2 * j + 1) * MX_NB + b] = (uint16_t)(w4[j] >> 16);
-            }
+        for (int it = 0; it < d / 64; ++it) {
+            const uint32_t o = (uint32_t)(tid + it * MX_THREADS) * 16u;
+            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.XT, o, 0, 0);
+            *reinterpret_cast<uint4 *>(Xs + o) = make_uint4(q[0], q[1], q[2], q[3]);
+        }
+        if (tg_lds) {
+            tg[tid] = ld32(R.K, 4u * tid);
+            tg[tid + MX_THREADS] = ld32(R.K, 4u * (tid + MX_THREADS));
         }
         for (int e = tid; e < d * MX_NLAB / 2; e += MX_THREADS) reinterpret_cast<uint32_t *>(T)[e] = 0u;
     }
-    // The batch's positives as keys (label << 6 | sample), sorted ascending
-    // (sort_keys512: a bitonic network, lane shuffles within waves and LDS across
-    // them; a label outside [0,L) becomes the largest key and
-    // is never matched).  Chunks of one workgroup come in ascending order, so
-    // a cursor that only moves forward finds each chunk's positives.
-    if (tg_lds) {
-        auto key_of = [&](int e) -> uint32_t {
-            if (e >= nnz) return 0xffffffffu;
-            const int32_t lb = a.tgt_lab[e];
-            const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
-            return lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B ? ((uint32_t)lb << 6) | (uint32_t)sb
-                                                                       : 0xffffffffu;
-        };
-        static_assert(MX_THREADS == 512, "sort_keys512 takes a 512-thread workgroup");
-        sort_keys512(tg, key_of(tid), key_of(tid + MX_THREADS), nnz, tid);
-    }
+    __syncthreads();
 
     // dX accumulators: 4 batch tiles x NT column tiles of 16 per wave (8 waves)
     const int cbase = wave * (d / 8);
@@ -647,15 +634,13 @@ bool sweep_mx_eligible(const Layer &ly, int B, int mode) {
 // the first stores its dW / dbias in the carry buffers, middle passes add to
 // them, and the last adds its share and applies Adam.  W, the moments and the
 // bias change only in the last pass, so every pass sees the step's old state.
-int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
-                    float *dbp, int *grid_out, int *passes_out) {
+int launch_sweep_mx(const SweepCall &c, const FastBufs &fb, int *grid_out, int *passes_out) {
     const Layer &ly = *c.layer;
     MxArgs a{};
     a.L = ly.L;
     a.d = ly.d;
     a.nnz = c.nnz;
     a.nchunks = (ly.L + MX_NLAB - 1) / MX_NLAB;
-    a.X = static_cast<const uint16_t *>(c.X);
     a.W = static_cast<uint16_t *>(ly.W);
     a.I = ly.I;
     a.bias = ly.bias;
@@ -663,13 +648,13 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.v = ly.v;
     a.bm = ly.bm;
     a.bv = ly.bv;
-    a.tgt_b = tgt_b;
+    a.tgt_b = fb.tgt_b;
     a.tgt_lab = c.tgt_lab;
     a.s = c.s;
     a.adam = c.adam;
-    a.dx_part = dx_part;
-    a.dwp = dwp;
-    a.dbp = dbp;
+    a.dx_part = fb.dx_part;
+    a.dwp = fb.dwp;
+    a.dbp = fb.dbp;
     a.Btot = c.B;
     a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
     const bool setf = c.set_n >= 1 && c.set_n <= MX_SET_NMAX && sweep_mx_lds(ly.d, true) <= 160 * 1024;
@@ -680,7 +665,6 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
     a.set_mask = c.set_mask;
     a.set_exhausted = c.set_exhausted;
     a.nb_mask = c.set_mask ? (uint32_t)(ly.L * MX_K) : 0u;
-    a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * MX_K * 2);
     a.idx16 = ly.idx16;
     a.nb_I = (uint32_t)(ly.L * MX_K * (ly.idx16 ? 2 : 4));
@@ -696,7 +680,9 @@ int launch_sweep_mx(const SweepCall &c, const int32_t *tgt_b, float *loss_part, 
         const int mode = passes == 1 ? MX_ONLY : p == 0 ? MX_FIRST : p == passes - 1 ? MX_LAST : MX_MIDDLE;
         a.b0 = p * MX_NB;
         a.B = std::min(MX_NB, c.B - a.b0);
-        a.loss_part = loss_part + (size_t)p * grid;
+        a.XT = fb.xt + (size_t)p * ly.d * MX_NB;
+        a.keys = fb.keys + (size_t)p * MX_TG_MAX;
+        a.loss_part = fb.loss_part + (size_t)p * grid;
         const bool kset = setf && (mode == MX_ONLY || mode == MX_LAST);
         const MxKernel kern = mx_kernel(ly.d / 128, mode, kset);
         const size_t shm = sweep_mx_lds(ly.d, kset);

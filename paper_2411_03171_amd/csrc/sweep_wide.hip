@@ -62,7 +62,8 @@ struct WdArgs {
     int64_t L;
     int32_t d, B, nnz;
     int64_t nchunks;
-    const uint16_t *X;
+    const uint16_t *XT;     // this pass's samples transposed, [d][16] (batch prep)
+    const uint32_t *keys;   // this pass's sorted positives, [1024] (nnz <= 1024)
     uint16_t *W;
     const int32_t *I;
     float *bias, *m, *v, *bm, *bv;
@@ -73,7 +74,7 @@ struct WdArgs {
     float *dx_part;
     // array sizes in bytes: the range of each buffer resource, and the offset
     // that the chunk loop uses for an access that must not happen
-    uint32_t nb_X, nb_W, nb_I, nb_m, nb_b;
+    uint32_t nb_W, nb_I, nb_m, nb_b;
     int32_t idx16;   // I holds uint16 indices
     // batch pass: samples b0 .. b0+B-1 of Btot; dW / dbias carried between
     // passes in dwp [L][64], dbp [L]
@@ -83,7 +84,7 @@ struct WdArgs {
 };
 
 struct Rsrcs {
-    Rsrc X, W, I, m, v, b, bm, bv, dwp, dbp;
+    Rsrc XT, K, W, I, m, v, b, bm, bv, dwp, dbp;
 };
 
 // G and T rows hold 16 bf16 (32 bytes = four 8-byte quarters).  A matrix-core
@@ -156,7 +157,8 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
     uint32_t *ymw = tg + 2 * wave;   // scan path: this wave's two rows' masks
 
     Rsrcs R;
-    R.X = make_rsrc(a.X, a.nb_X);
+    R.XT = make_rsrc(a.XT, (uint32_t)d * WD_XS);
+    R.K = make_rsrc(a.keys, tg_lds ? WD_TG_MAX * 4u : 0u);
     R.W = make_rsrc(a.W, a.nb_W);
     R.I = make_rsrc(a.I, a.nb_I);
     R.m = make_rsrc(a.m, a.nb_m);
@@ -170,39 +172,24 @@ __global__ void __launch_bounds__(WD_THREADS, 1) k_sweep_wide(const WdArgs a) {
     Prefetch pa, pb;
     prefetch<ADAM>(a, R, blockIdx.x, tid, lab, myslot, pa);
 
-    // stage the pass's samples transposed (sample fastest) and zero past B;
-    // clear T and G
+    // stage the pass's X tile (transposed and zero-padded past B by the batch
+    // prep) with 16-byte copies, its sorted positives, and clear T and G.  The
+    // positives are keys (label << 4 | sample), ascending (a label outside
+    // [0,L) is the largest key and is never matched).  Chunks of one
+    // workgroup come in ascending order, so a cursor that only moves forward
+    // finds each chunk's positives.
     {
-        uint16_t *X16 = reinterpret_cast<uint16_t *>(Xs);
-        const int b = lane & 15;
-        for (int gi = 4 * wave + (lane >> 4); gi < d / 8; gi += 4 * (WD_THREADS / 64)) {
-            const uint32_t ox = b < a.B ? (uint32_t)((a.b0 + b) * d + 8 * gi) * 2u : a.nb_X;
-            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.X, ox, 0, 0);
-            const uint32_t w4[4] = {q[0], q[1], q[2], q[3]};
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                X16[(8 * gi + 2 * j) * WD_NB + b] = (uint16_t)(w4[j] & 0xffffu);
-                X16[(8 * gi + 2 * j + 1) * WD_NB + b] = (uint16_t)(w4[j] >> 16);
-            }
+        for (int e = tid; e < d * WD_XS / 16; e += WD_THREADS) {
+            const auto q = __builtin_amdgcn_raw_buffer_load_b128(R.XT, 16u * e, 0, 0);
+            *reinterpret_cast<uint4 *>(Xs + 16 * e) = make_uint4(q[0], q[1], q[2], q[3]);
+        }
+        if (tg_lds) {
+            tg[tid] = ld32(R.K, 4u * tid);
+            tg[tid + WD_THREADS] = ld32(R.K, 4u * (tid + WD_THREADS));
         }
         uint32_t *TG = reinterpret_cast<uint32_t *>(T);
         for (int e = tid; e < (d * WD_NLAB + WD_NB * WD_NLAB) / 2; e += WD_THREADS) TG[e] = 0u;
-    }
-    // The pass's positives as keys (label << 4 | sample), sorted ascending
-    // (sort_keys512: a bitonic network, lane shuffles within waves and LDS across
-    // them; a label outside [0,L) becomes the largest key and
-    // is never matched).  Chunks of one workgroup come in ascending order, so
-    // a cursor that only moves forward finds each chunk's positives.
-    if (tg_lds) {
-        auto key_of = [&](int e) -> uint32_t {
-            if (e >= nnz) return 0xffffffffu;
-            const int32_t lb = a.tgt_lab[e];
-            const int32_t sb = a.tgt_b[e] - a.b0;   // sample within this pass
-            return lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < a.B ? ((uint32_t)lb << 4) | (uint32_t)sb
-                                                                       : 0xffffffffu;
-        };
-        static_assert(WD_THREADS == 512, "sort_keys512 takes a 512-thread workgroup");
-        sort_keys512(tg, key_of(tid), key_of(tid + WD_THREADS), nnz, tid);
     }
     __syncthreads();
 
@@ -492,15 +479,13 @@ bool sweep_wide_eligible(const Layer &ly, int mode) {
 // middle passes add to them, and the last adds its share and applies Adam.
 // W, the moments and the bias change only in the last pass, so every pass
 // sees the step's old state.
-int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part, float *dx_part, float *dwp,
-                      float *dbp, int *grid_out, int *passes_out) {
+int launch_sweep_wide(const SweepCall &c, const FastBufs &fb, int *grid_out, int *passes_out) {
     const Layer &ly = *c.layer;
     WdArgs a{};
     a.L = ly.L;
     a.d = ly.d;
     a.nnz = c.nnz;
     a.nchunks = (ly.L + WD_NLAB - 1) / WD_NLAB;
-    a.X = static_cast<const uint16_t *>(c.X);
     a.W = static_cast<uint16_t *>(ly.W);
     a.I = ly.I;
     a.bias = ly.bias;
@@ -508,16 +493,15 @@ int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part
     a.v = ly.v;
     a.bm = ly.bm;
     a.bv = ly.bv;
-    a.tgt_b = tgt_b;
+    a.tgt_b = fb.tgt_b;
     a.tgt_lab = c.tgt_lab;
     a.s = c.s;
     a.adam = c.adam;
-    a.dx_part = dx_part;
-    a.dwp = dwp;
-    a.dbp = dbp;
+    a.dx_part = fb.dx_part;
+    a.dwp = fb.dwp;
+    a.dbp = fb.dbp;
     a.Btot = c.B;
     a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
-    a.nb_X = (uint32_t)((size_t)c.B * ly.d * 2);
     a.nb_W = (uint32_t)(ly.L * WD_K * 2);
     a.idx16 = ly.idx16;
     a.nb_I = (uint32_t)(ly.L * WD_K * (ly.idx16 ? 2 : 4));
@@ -534,7 +518,9 @@ int launch_sweep_wide(const SweepCall &c, const int32_t *tgt_b, float *loss_part
         const int mode = passes == 1 ? PASS_ONLY : p == 0 ? PASS_FIRST : p == passes - 1 ? PASS_LAST : PASS_MIDDLE;
         a.b0 = p * WD_NB;
         a.B = std::min(WD_NB, c.B - a.b0);
-        a.loss_part = loss_part + (size_t)p * grid;
+        a.XT = fb.xt + (size_t)p * ly.d * WD_NB;
+        a.keys = fb.keys + (size_t)p * WD_TG_MAX;
+        a.loss_part = fb.loss_part + (size_t)p * grid;
         const WdKernel kern = wd_kernel(ly.d / 128, mode);
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
