@@ -43,24 +43,34 @@ __global__ void __launch_bounds__(BP_THREADS) k_batch_prep(const BatchPrepArgs a
         __shared__ int32_t smp[BP_KEYS];
         const int p = blockIdx.x;
         const int b0 = p * PB, Bp = min(PB, a.B - b0);
+        // the thread's two labels and the offsets of its samples b = tid,
+        // tid + 512 (B <= 1024), all loaded before the first barrier
+        const int32_t lb0 = tid < a.nnz ? a.lab[tid] : -1;
+        const int32_t lb1 = tid + BP_THREADS < a.nnz ? a.lab[tid + BP_THREADS] : -1;
+        int er[2][2] = {{0, 0}, {0, 0}};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int b = tid + h * BP_THREADS;
+            if (b < a.B) {
+                er[h][0] = max(0, min(a.off[b], a.nnz));
+                er[h][1] = max(er[h][0], min(a.off[b + 1], a.nnz));
+            }
+        }
         for (int e = tid; e < BP_KEYS; e += BP_THREADS) smp[e] = -1;
         __syncthreads();
         // the sample of each positive pair, e in [off[b], off[b+1])
-        for (int b = tid; b < a.B; b += BP_THREADS) {
-            const int e0 = max(0, min(a.off[b], a.nnz));
-            const int e1 = max(e0, min(a.off[b + 1], a.nnz));
-            for (int e = e0; e < e1; ++e) smp[e] = b;
-        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            for (int e = er[h][0]; e < er[h][1]; ++e) smp[e] = tid + h * BP_THREADS;
         __syncthreads();
-        auto key_of = [&](int e) -> uint32_t {
+        auto key_of = [&](int e, int32_t lb) -> uint32_t {
             if (e >= a.nnz) return 0xffffffffu;
-            const int32_t lb = a.lab[e];
             const int32_t sb = smp[e] - b0;
             return lb >= 0 && (int64_t)lb < a.L && sb >= 0 && sb < Bp ? ((uint32_t)lb << SB) | (uint32_t)sb
                                                                        : 0xffffffffu;
         };
         static_assert(BP_THREADS == 512, "sort_keys512 takes a 512-thread workgroup");
-        sort_keys512(tg, key_of(tid), key_of(tid + BP_THREADS), a.nnz, tid);
+        sort_keys512(tg, key_of(tid, lb0), key_of(tid + BP_THREADS, lb1), a.nnz, tid);
         int N = 64;
         while (N < a.nnz) N <<= 1;   // tg[0 .. N) is sorted
         uint32_t *out = a.keys + (size_t)p * BP_KEYS;
@@ -94,6 +104,7 @@ __global__ void __launch_bounds__(BP_THREADS) k_batch_prep(const BatchPrepArgs a
 
 int launch_batch_prep(const uint16_t *X, int32_t B, int32_t d, const int32_t *off, const int32_t *lab,
                       int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, hipStream_t st) {
+    if (B < 1 || B > 2 * BP_THREADS) return fail(FFSL_EINVAL, "batch prep: B = %d outside [1, %d]", B, 2 * BP_THREADS);
     BatchPrepArgs a{};
     a.X = X;
     a.off = off;

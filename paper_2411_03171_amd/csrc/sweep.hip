@@ -314,6 +314,21 @@ __global__ void k_targets_prep(const int32_t *off, int32_t B, int32_t nnz, int32
     for (int e = e0; e < e1; ++e) tgt_b[e] = b;
 }
 
+// loss (+)= s * sum of workgroup partials, in a fixed order (one workgroup of
+// 256 threads)
+__device__ __forceinline__ void loss_reduce_block(const float *part, int nparts, float s, float *out, int accum) {
+    __shared__ float lred[256];
+    float acc = 0.f;
+    for (int p = threadIdx.x; p < nparts; p += 256) acc += part[p];
+    lred[threadIdx.x] = acc;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if ((int)threadIdx.x < st) lred[threadIdx.x] += lred[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[0] = accum ? out[0] + s * lred[0] : s * lred[0];
+}
+
 // dX[e] (+)= sum over workgroup partials in workgroup order
 __global__ void k_dx_reduce(const float *part, int nparts, int64_t n, float *out, int accum) {
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
@@ -327,8 +342,15 @@ __global__ void k_dx_reduce(const float *part, int nparts, int64_t n, float *out
 // The same sum for n divisible by 4: a workgroup owns 64 consecutive
 // elements (16 float4 columns); its 16 lane groups take every 16th partial
 // with independent 16-byte loads, and a fixed tree in LDS adds the groups.
+// With lout set, one more workgroup past the dX ones reduces the loss
+// partials (loss_reduce_block), so one launch finishes the step.
 __global__ void __launch_bounds__(256) k_dx_reduce4(const float4 *part, int nparts, int64_t n4, float4 *out,
-                                                    int accum) {
+                                                    int accum, const float *lpart, int nl, float ls, float *lout,
+                                                    int laccum) {
+    if (lout && blockIdx.x == gridDim.x - 1) {
+        loss_reduce_block(lpart, nl, ls, lout, laccum);
+        return;
+    }
     __shared__ float4 red[16][16];
     const int eg = threadIdx.x & 15, pg = threadIdx.x >> 4;
     const int64_t e = (int64_t)blockIdx.x * 16 + eg;
@@ -364,17 +386,8 @@ __global__ void __launch_bounds__(256) k_dx_reduce4(const float4 *part, int npar
 }
 
 // loss (+)= s * sum of workgroup partials, fixed order
-__global__ void k_loss_reduce(const float *part, int nparts, float s, float *out, int accum) {
-    __shared__ float red[256];
-    float acc = 0.f;
-    for (int p = threadIdx.x; p < nparts; p += 256) acc += part[p];
-    red[threadIdx.x] = acc;
-    __syncthreads();
-    for (int st = 128; st > 0; st >>= 1) {
-        if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) out[0] = accum ? out[0] + s * red[0] : s * red[0];
+__global__ void __launch_bounds__(256) k_loss_reduce(const float *part, int nparts, float s, float *out, int accum) {
+    loss_reduce_block(part, nparts, s, out, accum);
 }
 
 template <int KM, int VT, int MODE>
@@ -510,20 +523,26 @@ int launch_sweep(const SweepCall &c) {
 int finish_sweep(const SweepCall &c, const float *loss_part, const float *dx_part, int nloss, int B, int d,
                  int ndx) {
     int rc;
-    if (c.loss_out) {
+    const int laccum = (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0;
+    const bool want_dx = c.mode != SWEEP_FWD && c.dX_out;
+    const int64_t n = (int64_t)B * d;
+    const bool dx4 = want_dx && n % 4 == 0 && (reinterpret_cast<uintptr_t>(c.dX_out) & 15u) == 0;
+    if (c.loss_out && !dx4) {
         hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, c.stream, loss_part, nloss, c.s, c.loss_out,
-                           (c.flags & FFSL_ACCUM_LOSS) ? 1 : 0);
+                           laccum);
         rc = check_launch("loss_reduce");
         if (rc) return rc;
     }
-    if (c.mode != SWEEP_FWD && c.dX_out) {
-        const int64_t n = (int64_t)B * d;
+    if (want_dx) {
         const int accum = (c.flags & FFSL_ACCUM_DX) ? 1 : 0;
-        if (n % 4 == 0 && (reinterpret_cast<uintptr_t>(c.dX_out) & 15u) == 0) {
+        if (dx4) {
+            // the loss partials ride along in one extra workgroup
             const int64_t n4 = n / 4;
-            hipLaunchKernelGGL(k_dx_reduce4, dim3((unsigned)((n4 + 15) / 16)), dim3(256), 0, c.stream,
+            const unsigned blocks = (unsigned)((n4 + 15) / 16) + (c.loss_out ? 1u : 0u);
+            hipLaunchKernelGGL(k_dx_reduce4, dim3(blocks), dim3(256), 0, c.stream,
                                reinterpret_cast<const float4 *>(dx_part), ndx, n4,
-                               reinterpret_cast<float4 *>(c.dX_out), accum);
+                               reinterpret_cast<float4 *>(c.dX_out), accum, loss_part, nloss, c.s, c.loss_out,
+                               laccum);
         } else {
             const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
             hipLaunchKernelGGL(k_dx_reduce, dim3(blocks), dim3(256), 0, c.stream, dx_part, ndx, n, c.dX_out,
