@@ -270,13 +270,46 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
             if (!tg_lds && tid < MX_NLAB * 2) ym[tid] = 0u;
         }
         prefetch<ADAM>(a, R, chunk + gridDim.x, tid, lab, u, Kown, nxt);
+        // The gathers read only X and the index rows this wave's own lanes
+        // staged above, so they need no barrier: issued here, their LDS
+        // latency runs on while the wave waits at the barrier below.
+        wave_lds_sync();
+        const int pc0 = c0, pc1 = c1;   // T columns written in the previous chunk
+        int rl = lab;            // the row of the chunk this lane serves
+        int k4 = Kp >> 2;        // quad order of this lane
+        // opaque per chunk, so the per-slot LDS addresses are formed where
+        // they are used instead of being held in registers across chunks
+        asm volatile("" : "+v"(rl), "+v"(k4));
+        // row data in the lane's slot order: register r <-> slot r ^ K (a row
+        // past L has zero offsets and weights)
+        uint32_t wp[MX_K / 2];
+        uint2 xg[MX_K];
+        const bool odd = (u & 1) != 0;
+        uint32_t wpair_own = 0u;
+#pragma unroll
+        for (int q = 0; q < MX_K / 4; ++q) {
+            const int qq = q ^ k4;   // registers 4q..4q+3 hold slots 4qq..4qq+3
+            const int4 iv = *reinterpret_cast<const int4 *>(Is + rl * MX_K + 4 * qq);
+            const uint2 wv = *reinterpret_cast<const uint2 *>(Ws + rl * (MX_K / 2) + 2 * qq);
+            if (q == 0) {   // the lane's own slots are registers 2*odd, 2*odd + 1
+                c0 = (odd ? iv.z : iv.x) / MX_XS;
+                c1 = (odd ? iv.w : iv.y) / MX_XS;
+                wpair_own = odd ? wv.y : wv.x;
+            }
+            xg[4 * q] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
+            xg[4 * q + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
+            xg[4 * q + 2] = *reinterpret_cast<const uint2 *>(Xs + iv.z + 8 * u);
+            xg[4 * q + 3] = *reinterpret_cast<const uint2 *>(Xs + iv.w + 8 * u);
+            wp[2 * q] = wv.x;
+            wp[2 * q + 1] = wv.y;
+        }
         __syncthreads();
         // Every wave has read the previous chunk's G and T fragments before the
         // barrier above, so this lane's T entries of that chunk can be cleared;
         // the entries of one row are only ever touched by the wave that owns
         // the row, in program order.
-        T[swz(c0, lab)] = 0;
-        T[swz(c1, lab)] = 0;
+        T[swz(pc0, lab)] = 0;
+        T[swz(pc1, lab)] = 0;
 
         // targets of this lane's row as a 64-bit sample mask
         uint64_t yrow = 0;
@@ -306,11 +339,6 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         }
 
         {
-            int rl = lab;            // the row of the chunk this lane serves
-            int k4 = Kp >> 2;        // quad order of this lane
-            // opaque per chunk, so the per-slot LDS addresses are formed where
-            // they are used instead of being held in registers across chunks
-            asm volatile("" : "+v"(rl), "+v"(k4));
             const int64_t l = l0 + rl;
             const bool valid = l < a.L;
             // the bias moments, used on lane u = 0 at the end of the row's work
@@ -329,29 +357,6 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                 dbprev = ldf(R.dbp, obm);
             }
 
-            // row data in the lane's slot order: register r <-> slot r ^ K (a row
-            // past L has zero offsets and weights)
-            uint32_t wp[MX_K / 2];
-            uint2 xg[MX_K];
-            const bool odd = (u & 1) != 0;
-            uint32_t wpair_own = 0u;
-#pragma unroll
-            for (int q = 0; q < MX_K / 4; ++q) {
-                const int qq = q ^ k4;   // registers 4q..4q+3 hold slots 4qq..4qq+3
-                const int4 iv = *reinterpret_cast<const int4 *>(Is + rl * MX_K + 4 * qq);
-                const uint2 wv = *reinterpret_cast<const uint2 *>(Ws + rl * (MX_K / 2) + 2 * qq);
-                if (q == 0) {   // the lane's own slots are registers 2*odd, 2*odd + 1
-                    c0 = (odd ? iv.z : iv.x) / MX_XS;
-                    c1 = (odd ? iv.w : iv.y) / MX_XS;
-                    wpair_own = odd ? wv.y : wv.x;
-                }
-                xg[4 * q] = *reinterpret_cast<const uint2 *>(Xs + iv.x + 8 * u);
-                xg[4 * q + 1] = *reinterpret_cast<const uint2 *>(Xs + iv.y + 8 * u);
-                xg[4 * q + 2] = *reinterpret_cast<const uint2 *>(Xs + iv.z + 8 * u);
-                xg[4 * q + 3] = *reinterpret_cast<const uint2 *>(Xs + iv.w + 8 * u);
-                wp[2 * q] = wv.x;
-                wp[2 * q + 1] = wv.y;
-            }
             // forward: repack (b, b+1) pairs of two slots into slot pairs
             float z[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
