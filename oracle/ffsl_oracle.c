@@ -67,7 +67,8 @@ EXPORT void ffslref_targets_dense(int64_t B, int64_t L, const int64_t *off,
     memset(y, 0, (size_t)(B * L));
     for (int64_t b = 0; b < B; ++b)
         for (int64_t e = off[b]; e < off[b + 1]; ++e)
-            y[b * L + lab[e]] = 1;
+            if (lab[e] >= 0 && lab[e] < L)   /* labels outside [0,L) are ignored */
+                y[b * L + lab[e]] = 1;
 }
 
 /* Binary cross-entropy with logits (the loss used for LF-AmazonTitles-131K,
@@ -551,7 +552,8 @@ EXPORT double ffslref_aux_bce(int64_t B, int64_t d, int64_t C, const double *X,
     double *dZ = (double *)malloc(sizeof(double) * (size_t)(B * C));
     for (int64_t b = 0; b < B; ++b)
         for (int64_t e = off[b]; e < off[b + 1]; ++e)
-            ya[b * C + (lab[e] % C)] = 1;
+            if (lab[e] >= 0)   /* negative labels are ignored */
+                ya[b * C + (lab[e] % C)] = 1;
     for (int64_t b = 0; b < B; ++b)
         for (int64_t c = 0; c < C; ++c) {
             double acc = 0.0;

@@ -69,6 +69,14 @@ def test_targets_dense_dedups(oracle):
     assert y.tolist() == [[1, 0, 1, 0, 0], [0, 0, 0, 0, 0], [0, 1, 0, 0, 1]]
 
 
+def test_targets_dense_ignores_labels_outside_range(oracle):
+    # the boundary's contract: labels outside [0,L) are ignored
+    off = np.array([0, 4, 6])
+    lab = np.array([-1, 5, 3, 7, -100, 0], dtype=np.int32)
+    y = oracle.targets_dense(2, 5, off, lab)
+    assert y.tolist() == [[0, 0, 0, 1, 0], [1, 0, 0, 0, 0]]
+
+
 # -------------------------------------------------------------------- BCE
 
 def test_bce_closed_forms(oracle):
