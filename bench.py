@@ -481,11 +481,12 @@ def main():
         ev.record(b, stream)
         torch.cuda.synchronize()
         set_ms.append(ev.elapsed_ms(a, b))
-    set_ms_med = sorted(set_ms)[len(set_ms) // 2]
     sb = set_bytes(w, vb, n_set)
-    set_gbs = sb / (set_ms_med * 1e-3) / 1e9
-    print("[bench] SET: %.3f ms median, %.0f GB/s algorithmic, exhausted rows %d" %
-          (set_ms_med, set_gbs, int(exhausted.cpu()[0])), file=sys.stderr, flush=True)
+    set_ms_med = sorted(set_ms)[len(set_ms) // 2] if set_ms else None
+    set_gbs = sb / (set_ms_med * 1e-3) / 1e9 if set_ms else None
+    if set_ms:
+        print("[bench] SET: %.3f ms median, %.0f GB/s algorithmic, exhausted rows %d" %
+              (set_ms_med, set_gbs, int(exhausted.cpu()[0])), file=sys.stderr, flush=True)
 
     # SET fused into a training step (one call) against a plain step, both
     # timed alone with events: the marginal cost of a SET step
@@ -505,10 +506,11 @@ def main():
         fused_ms.append(one_step(lambda: layer.train_step_set(X, off, lab, t=t, frac=w.set_frac, seed=args.seed,
                                                               set_round=1000 + r, loss_out=loss, dX_out=dX,
                                                               mask=False, exhausted_out=exhausted)))
-    plain_med = sorted(plain_ms)[len(plain_ms) // 2]
-    fused_med = sorted(fused_ms)[len(fused_ms) // 2]
-    print("[bench] step with SET in one call: %.3f ms median (plain step %.3f ms): SET adds %.3f ms" %
-          (fused_med, plain_med, fused_med - plain_med), file=sys.stderr, flush=True)
+    plain_med = sorted(plain_ms)[len(plain_ms) // 2] if plain_ms else None
+    fused_med = sorted(fused_ms)[len(fused_ms) // 2] if fused_ms else None
+    if fused_ms:
+        print("[bench] step with SET in one call: %.3f ms median (plain step %.3f ms): SET adds %.3f ms" %
+              (fused_med, plain_med, fused_med - plain_med), file=sys.stderr, flush=True)
 
     # the squared hinge (same step, other loss): scores near zero give a
     # dlogit everywhere; a bias of -4 puts every label without a positive in
@@ -527,8 +529,9 @@ def main():
     layer.bias.copy_(bias_saved)
     torch.cuda.synchronize()
     if args.hinge_reps > 0:
-        print("[bench] squared hinge step: %.3f ms (dense dlogits), %.3f ms (past the margin); BCE %.3f ms" %
-              (hinge["dense_dlogits"], hinge["past_margin"], plain_med), file=sys.stderr, flush=True)
+        print("[bench] squared hinge step: %.3f ms (dense dlogits), %.3f ms (past the margin); BCE %s ms" %
+              (hinge["dense_dlogits"], hinge["past_margin"], "%.3f" % plain_med if plain_med else "-"),
+              file=sys.stderr, flush=True)
 
     # inference over the whole label space: each sample's top 5 labels and
     # P@1..P@5 (the scores never reach memory)
@@ -683,13 +686,13 @@ def main():
             "frac": set_gbs / HBM_PEAK_GBS,
             "frac_of_copy": set_gbs / copy["gbs"] if copy else None,
             "prune_per_row": n_set,
-        },
+        } if set_ms else None,
         "set_in_step": {
             "ms_median": fused_med,
             "plain_step_ms_median": plain_med,
             "marginal_ms": fused_med - plain_med,
             "note": "ffsl_train_step_set: SET applied in the sweep that applies Adam",
-        },
+        } if fused_ms else None,
         "sqhinge_step": {
             "ms_median_dense_dlogits": hinge["dense_dlogits"],
             "ms_median_past_margin": hinge["past_margin"],
