@@ -599,9 +599,11 @@ def main():
         del layer16, I16
         torch.cuda.synchronize()
 
-    dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
-    print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
-          (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
+    dense = {"dense_gelu": None, "aux_head": None}
+    if args.dense_reps > 0:
+        dense = time_dense_parts(torch, ffsl, synth, ev, stream, dev, args.dense_reps)
+        print("[bench] dense GELU layer (C3 shape): %.1f us fwd+bwd; aux head (C5 shape): %.1f us" %
+              (dense["dense_gelu"]["us_median"], dense["aux_head"]["us_median"]), file=sys.stderr, flush=True)
 
     # the achievable streaming rate on this device: a plain 1 GiB device copy
     # (read + write), median of a few, event-timed
