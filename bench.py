@@ -169,7 +169,7 @@ def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
     ws5 = torch.empty(lib.ffsl_aux_workspace_bytes(B, d, C), dtype=torch.uint8, device=dev)
 
     def aux_step():
-        ffsl._check(lib.ffsl_aux_bce_fwd_bwd(p(X5), B, d, C, p(Wa), p(ca), p(offt), p(labt), len(lab),
+        ffsl._check(lib.ffsl_aux_bce_fwd_bwd(p(X5), B, d, C, w5.L, p(Wa), p(ca), p(offt), p(labt), len(lab),
                                              1.0 / B, p(loss), p(dWa), p(dca), p(dX5), None, 0, p(ws5),
                                              ws5.numel(), stream))
     us = median_us(aux_step)

@@ -91,11 +91,22 @@ FFSL_API int ffsl_version(void);
  * B_max samples with up to nnz_max positive (sample, label) pairs per batch.
  * Besides per-workgroup partial sums of the loss and dX (O(B_max * d)), the
  * fused step carries dW and dbias between passes over the batch in 4*(L*k + L)
- * bytes: for k = 32 and B_max > 64 (passes of 64 samples), and for k = 64,
- * d a multiple of 128 up to 2048, L < 2^24 and B_max > 16 (passes of 16).
+ * bytes: for k = 32, d a multiple of 128 up to 768, L < 2^25 and B_max > 64
+ * (passes of 64 samples), and for k = 64, d a multiple of 128 up to 2048,
+ * L < 2^24 and B_max > 16 (passes of 16).
  * Returns 0 for invalid shapes. */
 FFSL_API size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max,
                             int32_t nnz_max);
+
+/* As ffsl_workspace_bytes, for values of type value_dtype (FFSL_F32 or
+ * FFSL_BF16): the dW / dbias carry and the fast paths' batch buffers are
+ * counted only for the bf16 shapes that take a fused fast path (fan-in 32 with
+ * d a multiple of 128 up to 768 and L < 2^25; the fan-in-64 shapes above), so
+ * an fp32 layer, or a bf16 layer off those shapes, needs only the partial sums.
+ * ffsl_workspace_bytes is this call with FFSL_BF16 (an upper bound for both
+ * types).  Returns 0 for invalid shapes or types. */
+FFSL_API size_t ffsl_workspace_bytes_ex(int64_t L, int32_t d, int32_t k, int32_t value_dtype,
+                            int32_t B_max, int32_t nnz_max);
 
 /* Create a handle over caller-owned layer state (Sec. 2.2 storage; Sec. 2.2
  * notes that gradient and both Adam moments share the weights' index
@@ -334,16 +345,19 @@ FFSL_API size_t ffsl_aux_workspace_bytes(int32_t B_max, int32_t d, int32_t C);
  * so label l belongs to cluster l mod C), trained with its own BCE loss next
  * to the sparse layer's:
  *   Za[b,c] = ca[c] + sum_i X[b,i] Wa[i,c]
- *   ya[b,c] = 1 iff some positive l of sample b has l mod C == c
+ *   ya[b,c] = 1 iff some positive l of sample b has l mod C == c, over the
+ *             labels l in [0, n_labels): as in ffsl_forward_loss a label
+ *             outside that range is ignored (n_labels >= 1 is the sparse
+ *             layer's L)
  *   *loss_out = s * sum BCE-with-logits(Za, ya)    (+= with FFSL_ACCUM_LOSS)
  *   dZ = s * (sigmoid(Za) - ya)                    (fp32, bf16 for the products)
  *   dWa[i,c] = sum_b X[b,i] dZ[b,c];  dca[c] = sum_b dZ[b,c]
  *   dX[b,i] = sum_c dZ[b,c] Wa[i,c]                (+= with FFSL_ACCUM_DX)
  *   X [B,d] bf16; Wa [d,C] bf16; ca [C] fp32 nullable; tgt_off/tgt_lab as in
- *   ffsl_forward_loss (negative labels are ignored); loss_out, dca, dX_out,
+ *   ffsl_forward_loss; loss_out, dca, dX_out,
  *   logits_out (fp32 [B,C], for tests) nullable; dWa [d,C] fp32. */
 FFSL_API int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C,
-                         const void *Wa, const float *ca, const int32_t *tgt_off,
+                         int64_t n_labels, const void *Wa, const float *ca, const int32_t *tgt_off,
                          const int32_t *tgt_lab, int32_t nnz, float s, float *loss_out,
                          float *dWa, float *dca, float *dX_out, float *logits_out,
                          uint32_t flags, void *workspace, size_t workspace_bytes,

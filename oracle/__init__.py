@@ -69,7 +69,7 @@ def lib():
         L.ffslref_dense_gelu_fwd.restype = None
         L.ffslref_dense_gelu_bwd.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
         L.ffslref_dense_gelu_bwd.restype = None
-        L.ffslref_aux_bce.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, dbl, vp, vp, vp, vp]
+        L.ffslref_aux_bce.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, dbl, vp, vp, vp, vp]
         L.ffslref_aux_bce.restype = dbl
         L.ffslref_topk.argtypes = [i64, i64, vp, i64, vp, vp]
         L.ffslref_topk.restype = None
@@ -296,7 +296,9 @@ def dense_gelu_bwd(X, W1, A, dH):
     return dW1, dc, dX
 
 
-def aux_bce(X, Wa, ca, off, lab, s):
+def aux_bce(X, Wa, ca, off, lab, s, L):
+    """The auxiliary cluster head over the labels [0, L) (labels outside are
+    ignored), cluster(l) = l mod C."""
     X, Wa = _f64(X), _f64(Wa)
     B, d = X.shape
     C = Wa.shape[1]
@@ -306,7 +308,7 @@ def aux_bce(X, Wa, ca, off, lab, s):
     dWa = np.empty((d, C))
     dca = np.empty(C)
     dXa = np.empty((B, d))
-    loss = lib().ffslref_aux_bce(B, d, C, _p(X), _p(Wa), _p(cc), _p(off), _p(lab), float(s),
+    loss = lib().ffslref_aux_bce(B, d, C, int(L), _p(X), _p(Wa), _p(cc), _p(off), _p(lab), float(s),
                                  _p(Za), _p(dWa), _p(dca), _p(dXa))
     return dict(loss=loss, Za=Za, dWa=dWa, dca=dca, dXa=dXa)
 

@@ -539,11 +539,13 @@ EXPORT void ffslref_dense_gelu_bwd(int64_t B, int64_t din, int64_t dout,
  *     Za[b,c]  = ca[c] + sum_i X[b,i] * Wa[i,c]          (Wa is [d, C])
  *     ya[b,c]  = 1 iff some l in P_b has l mod C == c
  *     loss_a   = BCE-with-logits(Za, ya) summed, times s
+ * A label outside [0, L) is not a label of the layer and has no cluster: it
+ * is ignored, exactly as the sparse head's targets ignore it.
  *     dZa      = s * (sigmoid(Za) - ya)
  *     dWa[i,c] = sum_b X[b,i] dZa[b,c];  dca[c] = sum_b dZa[b,c]
  *     dXa[b,i] = sum_c dZa[b,c] Wa[i,c].
  * Returns loss_a.  ca, dca may be NULL.                                      */
-EXPORT double ffslref_aux_bce(int64_t B, int64_t d, int64_t C, const double *X,
+EXPORT double ffslref_aux_bce(int64_t B, int64_t d, int64_t C, int64_t L, const double *X,
                               const double *Wa, const double *ca,
                               const int64_t *off, const int32_t *lab, double s,
                               double *Za, double *dWa, double *dca, double *dXa)
@@ -552,7 +554,7 @@ EXPORT double ffslref_aux_bce(int64_t B, int64_t d, int64_t C, const double *X,
     double *dZ = (double *)malloc(sizeof(double) * (size_t)(B * C));
     for (int64_t b = 0; b < B; ++b)
         for (int64_t e = off[b]; e < off[b + 1]; ++e)
-            if (lab[e] >= 0)   /* negative labels are ignored */
+            if (lab[e] >= 0 && lab[e] < L)   /* labels outside [0,L) are ignored */
                 ya[b * C + (lab[e] % C)] = 1;
     for (int64_t b = 0; b < B; ++b)
         for (int64_t c = 0; c < C; ++c) {

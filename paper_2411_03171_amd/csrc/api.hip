@@ -46,9 +46,13 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int max_parts_for(int num_cu) { return std::max(1, std::min(2 * num_cu, 1024)); }
 
-WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts) {
+WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t vt, int32_t B_max, int32_t nnz_max, int max_parts) {
     WsLayout w{};
-    const bool wide = wide_shape(L, d, k);
+    // the fused fast paths (bf16 only) and their buffers: the same shape
+    // predicates as their dispatch (sweep_mx_eligible, sweep_wide_eligible)
+    const bool bf16 = vt == FFSL_BF16;
+    const bool wide = bf16 && wide_shape(L, d, k);
+    const bool mx = bf16 && !wide && mx_shape(L, d, k);
     const int pass_b = wide ? WD_PASS_B : MX_PASS_B;
     const int passes = (B_max + pass_b - 1) / pass_b;
     size_t off = 0;
@@ -58,12 +62,12 @@ WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_m
     off = align256(off + sizeof(int32_t) * (size_t)std::max(nnz_max, 1));
     w.dx_part = off;
     off = align256(off + sizeof(float) * (size_t)max_parts * (size_t)B_max * (size_t)d);
-    w.has_partial = (k == 32 && B_max > MX_PASS_B) || (wide && B_max > WD_PASS_B);
+    w.has_partial = (mx && B_max > MX_PASS_B) || (wide && B_max > WD_PASS_B);
     w.dwp = off;
     if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L * (size_t)k);
     w.dbp = off;
     if (w.has_partial) off = align256(off + sizeof(float) * (size_t)L);
-    w.has_xt = wide || (k == 32 && d % 128 == 0 && d >= 128 && d <= 768);
+    w.has_xt = wide || mx;
     w.keys = off;
     if (w.has_xt) off = align256(off + sizeof(uint32_t) * 1024 * (size_t)passes);
     w.xt = off;
@@ -153,11 +157,19 @@ const char *ffsl_last_error(void) { return g_err.c_str(); }
 
 int ffsl_version(void) { return 100; }
 
-size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max) {
+size_t ffsl_workspace_bytes_ex(int64_t L, int32_t d, int32_t k, int32_t value_dtype, int32_t B_max,
+                               int32_t nnz_max) {
     if (check_shape(L, d, k, B_max, nnz_max)) return 0;
+    if (value_dtype != FFSL_F32 && value_dtype != FFSL_BF16) return 0;
     int cu = 0, dev = 0;
     if (device_cu_count(&cu, &dev)) return 0;
-    return ws_layout(L, d, k, B_max, nnz_max, max_parts_for(cu)).total;
+    return ws_layout(L, d, k, value_dtype, B_max, nnz_max, max_parts_for(cu)).total;
+}
+
+size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max) {
+    // without the value type: the bf16 layout, which holds every buffer an
+    // fp32 layer of the same shape needs
+    return ffsl_workspace_bytes_ex(L, d, k, FFSL_BF16, B_max, nnz_max);
 }
 
 int ffsl_create_layer_ex(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int32_t value_dtype,
@@ -187,7 +199,7 @@ int ffsl_create_layer_ex(ffsl_layer **out, int64_t L, int32_t d, int32_t k, int3
     rc = device_cu_count(&cu, &dev);
     if (rc) return rc;
     const int parts = max_parts_for(cu);
-    const WsLayout wl = ws_layout(L, d, k, B_max, nnz_max, parts);
+    const WsLayout wl = ws_layout(L, d, k, value_dtype, B_max, nnz_max, parts);
     if (workspace_bytes < wl.total)
         return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, wl.total);
     ffsl_layer *h = new (std::nothrow) ffsl_layer;
@@ -490,7 +502,8 @@ size_t ffsl_aux_workspace_bytes(int32_t B_max, int32_t d, int32_t C) {
     return aux_ws(B_max, d, C).total;
 }
 
-int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C, const void *Wa, const float *ca,
+int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C, int64_t n_labels, const void *Wa,
+                         const float *ca,
                          const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz, float s, float *loss_out,
                          float *dWa, float *dca, float *dX_out, float *logits_out, uint32_t flags, void *workspace,
                          size_t workspace_bytes, void *stream) {
@@ -502,6 +515,7 @@ int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C, const v
     if (!tgt_off) return fail(FFSL_EINVAL, "tgt_off is null");
     if (nnz < 0) return fail(FFSL_EINVAL, "nnz must be >= 0");
     if (nnz > 0 && !tgt_lab) return fail(FFSL_EINVAL, "tgt_lab is null");
+    if (n_labels < 1) return fail(FFSL_EINVAL, "n_labels must be >= 1 (got %lld)", (long long)n_labels);
     if (!dWa) return fail(FFSL_EINVAL, "dWa is required");
     if (!workspace) return fail(FFSL_EINVAL, "workspace is null");
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
@@ -509,8 +523,8 @@ int ffsl_aux_bce_fwd_bwd(const void *X, int32_t B, int32_t d, int32_t C, const v
     const size_t need = aux_ws(B, d, C).total;
     if (workspace_bytes < need)
         return fail(FFSL_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
-    return launch_aux_bce(static_cast<const uint16_t *>(X), B, d, C, static_cast<const uint16_t *>(Wa), ca, tgt_off,
-                          tgt_lab, nnz, s, loss_out, dWa, dca, dX_out, logits_out, (flags & FFSL_ACCUM_DX) != 0,
+    return launch_aux_bce(static_cast<const uint16_t *>(X), B, d, C, n_labels, static_cast<const uint16_t *>(Wa), ca,
+                          tgt_off, tgt_lab, nnz, s, loss_out, dWa, dca, dX_out, logits_out, (flags & FFSL_ACCUM_DX) != 0,
                           (flags & FFSL_ACCUM_LOSS) != 0, static_cast<char *>(workspace),
                           static_cast<hipStream_t>(stream));
 }

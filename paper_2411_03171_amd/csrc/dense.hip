@@ -223,7 +223,8 @@ __global__ void __launch_bounds__(256) k_gelu_bwd_cols(const float *A, const flo
 // blocks in order.
 constexpr int BCE_ROWS = 32;
 __global__ void __launch_bounds__(256) k_bce_cols(const float *P, int S, int B, int N, const float *bias,
-                                                  const int32_t *off, const int32_t *lab, float sc, uint16_t *G16,
+                                                  const int32_t *off, const int32_t *lab, int64_t n_labels,
+                                                  float sc, uint16_t *G16,
                                                   float *csum_part, float *Zout, float *loss_part) {
     __shared__ float red[8][33];
     __shared__ float lred[256];
@@ -233,14 +234,14 @@ __global__ void __launch_bounds__(256) k_bce_cols(const float *P, int S, int B, 
     const int64_t MN = (int64_t)B * N;
     const int rb0 = blockIdx.y * BCE_ROWS, rb1 = min(B, rb0 + BCE_ROWS);
     // cluster targets: bit c of ym[r] iff some positive l of sample rb0 + r has
-    // l mod N == blockIdx.x * 32 + c (negative labels are ignored)
+    // l mod N == blockIdx.x * 32 + c (labels outside [0, n_labels) are ignored)
     if (threadIdx.x < BCE_ROWS) ym[threadIdx.x] = 0u;
     __syncthreads();
     {
         const int e0 = off[rb0], e1 = off[rb1];
         for (int e = e0 + (int)threadIdx.x; e < e1; e += 256) {
             const int l = lab[e];
-            if (l < 0) continue;
+            if (l < 0 || l >= n_labels) continue;
             const int cc = l % N - blockIdx.x * 32;
             if (cc < 0 || cc >= 32) continue;
             int r = 0;   // the sample of entry e: the last row with off[row] <= e
@@ -502,7 +503,7 @@ int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uin
     return check_launch("split_sum");
 }
 
-int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, const float *ca,
+int launch_aux_bce(const uint16_t *X, int B, int d, int C, int64_t n_labels, const uint16_t *Wa, const float *ca,
                    const int32_t *off, const int32_t *lab, int nnz, float s, float *loss, float *dWa, float *dca,
                    float *dX, float *Zout, bool accum_dx, bool accum_loss, char *ws, hipStream_t st) {
     const AuxWs w = aux_ws(B, d, C);
@@ -528,7 +529,8 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, c
     if (rc) return rc;
     const int eblocks = (C + 31) / 32, rblocks = (B + BCE_ROWS - 1) / BCE_ROWS;
     float *cp = reinterpret_cast<float *>(ws + w.csum_part);
-    hipLaunchKernelGGL(k_bce_cols, dim3(eblocks, rblocks), dim3(256), 0, st, zp, Sf, B, C, ca, off, lab, s, dz16,
+    hipLaunchKernelGGL(k_bce_cols, dim3(eblocks, rblocks), dim3(256), 0, st, zp, Sf, B, C, ca, off, lab, n_labels,
+                       s, dz16,
                        cp, Zout, lp);
     rc = check_launch("bce_cols");
     if (rc) return rc;

@@ -39,13 +39,19 @@ struct WsLayout {
     bool has_xt;        // the shape may take a fused fast path (keys, xt allocated)
     size_t total;
 };
-WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t B_max, int32_t nnz_max, int max_parts);
+// the workspace of a layer with values of type vt (FFSL_F32 / FFSL_BF16): the
+// fast paths' buffers are carved only for shapes that can take a fast path
+WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t vt, int32_t B_max, int32_t nnz_max, int max_parts);
 // samples per pass of the fused fast path
 constexpr int MX_PASS_B = 64;   // samples per pass of the fan-in-32 fast path
 constexpr int WD_PASS_B = 16;   // samples per pass of the wide fan-in-64 fast path
 // layers whose shape the wide fan-in-64 fast path serves (bf16 values)
 inline bool wide_shape(int64_t L, int32_t d, int32_t k) {
     return k == 64 && d % 128 == 0 && d >= 128 && d <= 2048 && L < ((int64_t)1 << 24);
+}
+// layers whose shape the fan-in-32 fast path serves (bf16 values)
+inline bool mx_shape(int64_t L, int32_t d, int32_t k) {
+    return k == 32 && d % 128 == 0 && d >= 128 && d <= 768 && L < ((int64_t)1 << 25);
 }
 int max_parts_for(int num_cu);
 
@@ -191,7 +197,7 @@ int launch_dense_gelu_fwd(const uint16_t *X, int B, int din, int dout, const uin
 int launch_dense_gelu_bwd(const uint16_t *X, int B, int din, int dout, const uint16_t *W1, const float *A,
                           const float *dH, float *dW1, float *dc, float *dX, bool accum, char *ws,
                           hipStream_t st);
-int launch_aux_bce(const uint16_t *X, int B, int d, int C, const uint16_t *Wa, const float *ca,
+int launch_aux_bce(const uint16_t *X, int B, int d, int C, int64_t n_labels, const uint16_t *Wa, const float *ca,
                    const int32_t *off, const int32_t *lab, int nnz, float s, float *loss, float *dWa, float *dca,
                    float *dX, float *Zout, bool accum_dx, bool accum_loss, char *ws, hipStream_t st);
 

@@ -9,10 +9,14 @@
 //   - the batch is cut into tiles of Bt samples; a tile of X is staged in LDS
 //     as fp32 [Bt][d] so every gather X[b, I[l,j]] is an LDS read;
 //   - dX contributions of a tile are accumulated in an LDS fp32 [Bt][d]
-//     array with LDS float atomics and flushed, at a tile switch and at the
+//     array with LDS float adds and flushed, at a tile switch and at the
 //     end, into a per-workgroup partial; a separate kernel sums the partials
-//     in workgroup order.  Tile order alternates between consecutive chunks
-//     so a chunk starts on the tile the previous one ended with.
+//     in workgroup order.  The four waves add their contributions of a
+//     sample one after the other (a barrier between them), and the adds of
+//     one wave instruction that meet at one address are applied in lane
+//     order, so every sum is formed in the same order in every run.  Tile
+//     order alternates between consecutive chunks so a chunk starts on the
+//     tile the previous one ended with.
 //   - the loss is a per-thread sum reduced per workgroup in a fixed tree and
 //     then over workgroups in order.
 #include "ffsl_internal.h"
@@ -218,8 +222,9 @@ __global__ void __launch_bounds__(SW_THREADS) k_sweep(const SweepArgs a) {
                 }
             }
             __syncthreads();
-            if (valid) {
-                for (int bb = 0; bb < bn; ++bb) {
+            for (int bb = 0; bb < bn; ++bb) {
+                float g = 0.f;
+                if (valid) {
                     const float *xr = Xs + (size_t)bb * d;
                     float xg[KM];
                     float z = bl;
@@ -243,16 +248,23 @@ __global__ void __launch_bounds__(SW_THREADS) k_sweep(const SweepArgs a) {
                     if (MODE != SWEEP_FWD) {
                         const float r = 1.f / (1.f + e);
                         const float sig = z >= 0.f ? r : e * r;
-                        const float g = a.hinge ? -2.f * a.s * yh * hh : a.s * (sig - y);
+                        g = a.hinge ? -2.f * a.s * yh * hh : a.s * (sig - y);
                         db += g;
-                        float *dxr = dXs + (size_t)bb * d;
 #pragma unroll
-                        for (int j = 0; j < KM; ++j) {
-                            if (j < k) {
-                                dw[j] = fmaf(g, xg[j], dw[j]);
-                                atomicAdd(&dxr[idx[j]], g * w[j]);
-                            }
+                        for (int j = 0; j < KM; ++j)
+                            if (j < k) dw[j] = fmaf(g, xg[j], dw[j]);
+                    }
+                }
+                if (MODE != SWEEP_FWD) {
+                    // dX: the waves add in turn (fixed order; see the header)
+                    float *dxr = dXs + (size_t)bb * d;
+                    for (int wv = 0; wv < SW_THREADS / 64; ++wv) {
+                        if (valid && (tid >> 6) == wv) {
+#pragma unroll
+                            for (int j = 0; j < KM; ++j)
+                                if (j < k) atomicAdd(&dxr[idx[j]], g * w[j]);
                         }
+                        __syncthreads();
                     }
                 }
             }
@@ -437,7 +449,7 @@ int launch_sweep(const SweepCall &c) {
     if (T > SW_MAXT) return fail(FFSL_EUNSUPPORTED, "too many batch tiles (%d)", T);
     const size_t shm = (size_t)Bt * per_b + ym_bytes;
 
-    const WsLayout wl = ws_layout(ly.L, d, ly.k, ly.B_max, ly.nnz_max, ly.max_parts);
+    const WsLayout wl = ws_layout(ly.L, d, ly.k, ly.vt, ly.B_max, ly.nnz_max, ly.max_parts);
     SweepArgs a{};
     a.L = ly.L;
     a.d = d;

@@ -628,8 +628,9 @@ size_t sweep_mx_lds(int d, bool setf = false) {
 }  // namespace
 
 bool sweep_mx_eligible(const Layer &ly, int B, int mode) {
-    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && ly.k == MX_K && B <= FFSL_MAX_B && ly.d % 128 == 0 &&
-           ly.d >= 128 && ly.d <= 128 * MX_NT_MAX && ly.L < ((int64_t)1 << 25) && sweep_mx_lds(ly.d) <= 160 * 1024;
+    static_assert(MX_K == 32 && MX_NT_MAX * 128 == 768, "the shape predicate mx_shape");
+    return mode == SWEEP_FUSED && ly.vt == FFSL_BF16 && mx_shape(ly.L, ly.d, ly.k) && B <= FFSL_MAX_B &&
+           sweep_mx_lds(ly.d) <= 160 * 1024;
 }
 
 // With c.set_n in [1, MX_SET_NMAX] the pass that applies Adam also applies

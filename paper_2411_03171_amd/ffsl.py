@@ -26,6 +26,7 @@ SIGNATURES = {
     "ffsl_last_error": (ctypes.c_char_p, []),
     "ffsl_version": (_int, []),
     "ffsl_workspace_bytes": (_sz, [_i64, _i32, _i32, _i32, _i32]),
+    "ffsl_workspace_bytes_ex": (_sz, [_i64, _i32, _i32, _i32, _i32, _i32]),
     "ffsl_create_layer": (_int, [ctypes.POINTER(_vp), _i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp, _sz, _i32, _i32]),
     "ffsl_create_layer_ex": (_int, [ctypes.POINTER(_vp), _i64, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp,
@@ -49,7 +50,7 @@ SIGNATURES = {
     "ffsl_dense_gelu_bwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp, _sz,
                                    _vp]),
     "ffsl_aux_workspace_bytes": (_sz, [_i32, _i32, _i32]),
-    "ffsl_aux_bce_fwd_bwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _f32, _vp, _vp, _vp,
+    "ffsl_aux_bce_fwd_bwd": (_int, [_vp, _i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _i32, _f32, _vp, _vp, _vp,
                                     _vp, _vp, _u32, _vp, _sz, _vp]),
     "ffsl_adam_dense": (_int, [_vp, _i32, _vp, _vp, _vp, _i64, _i64, _f32, _f32, _f32, _f32, _f32, _vp]),
 }
@@ -152,7 +153,7 @@ class SparseLayer:
         torch = self.torch
         lib = load()
         self.d = int(d)
-        nbytes = lib.ffsl_workspace_bytes(self.L, self.d, self.k, self.B_max, self.nnz_max)
+        nbytes = lib.ffsl_workspace_bytes_ex(self.L, self.d, self.k, self.vt, self.B_max, self.nnz_max)
         if nbytes == 0:
             raise FfslError(FFSL_EINVAL, lib.ffsl_last_error().decode())
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.W.device)
@@ -370,8 +371,10 @@ def dense_gelu_bwd(X, W1, A, dH, want_dc=True, dX_out=None, flags=0):
     return dW1, dc, dX
 
 
-def aux_bce_fwd_bwd(X, Wa, ca, off, lab, s=None, want_logits=False, dX_out=None, loss_out=None, flags=0):
-    """Loss, dWa, dca, dX (and optionally the logits) of the auxiliary cluster head."""
+def aux_bce_fwd_bwd(X, Wa, ca, off, lab, n_labels, s=None, want_logits=False, dX_out=None, loss_out=None,
+                    flags=0):
+    """Loss, dWa, dca, dX (and optionally the logits) of the auxiliary cluster
+    head over the labels [0, n_labels) (the sparse layer's L)."""
     import torch
     lib = load()
     _bf16_2d(X, "X")
@@ -389,7 +392,7 @@ def aux_bce_fwd_bwd(X, Wa, ca, off, lab, s=None, want_logits=False, dX_out=None,
     if ws_bytes == 0:
         raise FfslError(FFSL_EINVAL, lib.ffsl_last_error().decode())
     ws = _workspace(torch, ws_bytes, dev)
-    _check(lib.ffsl_aux_bce_fwd_bwd(_ptr(X), B, d, C, _ptr(Wa), _ptr(ca), _ptr(off), _ptr(lab), int(lab.numel()),
+    _check(lib.ffsl_aux_bce_fwd_bwd(_ptr(X), B, d, C, int(n_labels), _ptr(Wa), _ptr(ca), _ptr(off), _ptr(lab), int(lab.numel()),
                                     float(s), _ptr(loss), _ptr(dWa), _ptr(dca), _ptr(dX), _ptr(Z), flags,
                                     _ptr(ws), ws.numel(), _stream(torch)))
     return loss, dWa, dca, dX, Z

@@ -82,7 +82,7 @@ class Model:
             w = schedule.aux_weight(epoch, self.aux_w0, self.aux_cutoff_epoch)
             if w > 0.0:
                 _, dWa, dca, dX, _ = ffsl.aux_bce_fwd_bwd(
-                    X, self.Wa, self.ca, off, lab, s=w / X.shape[0], dX_out=dX, loss_out=loss,
+                    X, self.Wa, self.ca, off, lab, sp.L, s=w / X.shape[0], dX_out=dX, loss_out=loss,
                     flags=ffsl.FFSL_ACCUM_DX | ffsl.FFSL_ACCUM_LOSS)
                 ffsl.adam_dense(self.Wa, dWa, self.mWa, self.vWa, t, lr=self.lr_aux, wd=self.wd_aux)
                 if self.ca is not None:

@@ -97,13 +97,13 @@ def test_aux_bce_fwd_bwd(torch_cuda, case):
     ca = (rng.standard_normal(C) * 0.1).astype(np.float32)
     off, lab = synth.gen_targets(rng, B, L, mean_pos, 1.1)
     s = 1.0 / B
-    ref = oracle.aux_bce(_f64(X), _f64(Wa), ca.astype(np.float64), off, lab, s)
+    ref = oracle.aux_bce(_f64(X), _f64(Wa), ca.astype(np.float64), off, lab, s, L)
     dev = "cuda:0"
     Xt, Wt = to_torch_values(X, "bf16", dev), to_torch_values(Wa, "bf16", dev)
     offt = torch.from_numpy(off.astype(np.int32)).to(dev)
     labt = torch.from_numpy(lab.astype(np.int32)).to(dev)
     note("aux bce %s B=%d d=%d C=%d nnz=%d" % (name, B, d, C, len(lab)))
-    loss, dWa, dca, dX, Z = ffsl.aux_bce_fwd_bwd(Xt, Wt, torch.from_numpy(ca).to(dev), offt, labt, s,
+    loss, dWa, dca, dX, Z = ffsl.aux_bce_fwd_bwd(Xt, Wt, torch.from_numpy(ca).to(dev), offt, labt, L, s,
                                                  want_logits=True)
     torch.cuda.synchronize()
     assert_close(Z.cpu().numpy(), ref["Za"], RTOL_F32, "Za")
@@ -116,7 +116,7 @@ def test_aux_bce_fwd_bwd(torch_cuda, case):
     Rt = torch.from_numpy(R).to(dev)
     l0 = torch.full((1,), 3.5, dtype=torch.float32, device=dev)
     note("aux bce accumulate %s" % name)
-    ffsl.aux_bce_fwd_bwd(Xt, Wt, torch.from_numpy(ca).to(dev), offt, labt, s, dX_out=Rt, loss_out=l0,
+    ffsl.aux_bce_fwd_bwd(Xt, Wt, torch.from_numpy(ca).to(dev), offt, labt, L, s, dX_out=Rt, loss_out=l0,
                          flags=ffsl.FFSL_ACCUM_DX | ffsl.FFSL_ACCUM_LOSS)
     torch.cuda.synchronize()
     assert_close(Rt.cpu().numpy() - R, ref["dXa"], RTOL_BF16, "dXa accumulated")
@@ -132,15 +132,41 @@ def test_aux_bce_no_positives_and_no_bias(torch_cuda):
     Wa = synth.make_dense(rng, d, C)
     off = np.zeros(B + 1, dtype=np.int64)
     lab = np.zeros(0, dtype=np.int32)
-    ref = oracle.aux_bce(_f64(X), _f64(Wa), None, off, lab, 0.5)
+    ref = oracle.aux_bce(_f64(X), _f64(Wa), None, off, lab, 0.5, 100)
     dev = "cuda:0"
     note("aux bce empty targets")
     loss, dWa, dca, dX, _ = ffsl.aux_bce_fwd_bwd(
         to_torch_values(X, "bf16", dev), to_torch_values(Wa, "bf16", dev), None,
-        torch.zeros(B + 1, dtype=torch.int32, device=dev), torch.zeros(0, dtype=torch.int32, device=dev), 0.5)
+        torch.zeros(B + 1, dtype=torch.int32, device=dev), torch.zeros(0, dtype=torch.int32, device=dev), 100, 0.5)
     torch.cuda.synchronize()
     assert dca is None
     assert_close(np.array([float(loss.cpu()[0])]), np.array([ref["loss"]]), RTOL_F32, "loss")
+    assert_close(dWa.cpu().numpy(), ref["dWa"], RTOL_BF16, "dWa")
+    assert_close(dX.cpu().numpy(), ref["dXa"], RTOL_BF16, "dXa")
+
+
+def test_aux_bce_labels_outside_the_layer(torch_cuda):
+    """Labels outside [0, n_labels) (negative, n_labels itself, beyond) are
+    ignored by the auxiliary head, as by the sparse layer."""
+    torch = torch_cuda
+    from paper_2411_03171_amd import ffsl
+    rng = np.random.default_rng(9)
+    B, d, C, L = 6, 64, 24, 50
+    X = _x(rng, B, d)
+    Wa = synth.make_dense(rng, d, C)
+    ca = (rng.standard_normal(C) * 0.1).astype(np.float32)
+    off = np.array([0, 3, 4, 4, 7, 9, 12], dtype=np.int64)
+    lab = np.array([5, 50, -1, 73, 49, 0, 2**31 - 1, 24, 51, -2**31, 26, 99], dtype=np.int32)
+    s = 1.0 / B
+    ref = oracle.aux_bce(_f64(X), _f64(Wa), ca.astype(np.float64), off, lab, s, L)
+    dev = "cuda:0"
+    note("aux bce labels outside [0, L)")
+    loss, dWa, dca, dX, Z = ffsl.aux_bce_fwd_bwd(
+        to_torch_values(X, "bf16", dev), to_torch_values(Wa, "bf16", dev), torch.from_numpy(ca).to(dev),
+        torch.from_numpy(off.astype(np.int32)).to(dev), torch.from_numpy(lab).to(dev), L, s, want_logits=True)
+    torch.cuda.synchronize()
+    assert_close(np.array([float(loss.cpu()[0])]), np.array([ref["loss"]]), RTOL_F32, "loss")
+    assert_close(dca.cpu().numpy(), ref["dca"], RTOL_F32, "dca")
     assert_close(dWa.cpu().numpy(), ref["dWa"], RTOL_BF16, "dWa")
     assert_close(dX.cpu().numpy(), ref["dXa"], RTOL_BF16, "dXa")
 

@@ -1,17 +1,20 @@
-"""16-bit indices (ffsl_create_layer_ex with FFSL_IDX_U16): every call on a
-layer whose I is uint16 must give the results of the same layer with int32
-indices -- the storage differs, the arithmetic does not.  Compared bit for bit
-(weights, indices, moments, bias, masks, loss, dX), except dX and the loss of
-the general path, whose LDS float atomics sum in a varying order (there the
-bf16 or fp32 bar).  Shapes: the fan-in 32 fast path in one and several batch
+"""16-bit indices (ffsl_create_layer_ex with FFSL_IDX_U16, Sec. 2.2's
+16-bit index storage).  Against the oracle directly: the u16 layer's training
+step (fused and unfused), its SET in both prune modes and the fused step with
+SET (bit-exact on every row), and its top-k inference.  Against the same
+layer with int32 indices: every call must give the same results -- the
+storage differs, the arithmetic does not.  Compared bit for bit
+(weights, indices, moments, bias, masks, loss, dX): every path forms its sums
+in a fixed order.  Shapes: the fan-in 32 fast path in one and several batch
 passes with and without fused SET, the wide fan-in 64 path, the general path
 (bf16 at width 320, fp32), SET in both prune modes, top-k inference."""
 import numpy as np
 import pytest
 
+import oracle
 from paper_2411_03171_amd import synth
 from tests.parity import (RTOL_BF16, RTOL_F32, assert_close, batch_to_gpu, from_torch_bits, note,
-                          to_torch_values)
+                          to_torch_values, values_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -20,9 +23,9 @@ CASES = {
     "c4s": (synth.scaled(W1["c4_bf16_L3M"], L=3001, name="c4s"), True),
     "mx200": (synth.scaled(W1["c4_bf16_L3M"], L=777, B=200, name="mx200"), True),
     "w1024": (synth.scaled(W1["c3_inter2048_L1M"], L=777, d=1024, B=37, name="w1024"), True),
-    "mx320": (synth.scaled(W1["c4_bf16_L3M"], L=1003, d=320, B=37, name="mx320"), False),
-    "c1": (W1["c1_fp32_L4096"], False),
-    "k7": (synth.scaled(W1["c1_fp32_L4096"], L=500, d=40, k=7, B=9, name="k7"), False),
+    "mx320": (synth.scaled(W1["c4_bf16_L3M"], L=1003, d=320, B=37, name="mx320"), True),
+    "c1": (W1["c1_fp32_L4096"], True),
+    "k7": (synth.scaled(W1["c1_fp32_L4096"], L=500, d=40, k=7, B=9, name="k7"), True),
 }
 
 
@@ -103,14 +106,7 @@ def test_idx16_unfused_calls_equal_int32(name):
         torch.cuda.synchronize()
         runs.append(_snap(layer, w, {"z": z.cpu().numpy(), "loss": loss.cpu().numpy(), "dX": dX.cpu().numpy(),
                                      "dW": dW}))
-    # the unfused backward accumulates dW and dX with atomics on the general path
-    rtol = RTOL_F32 if w.value == "f32" else RTOL_BF16
-    for key in ("dW",):
-        assert_close(runs[1][key], runs[0][key].astype(np.float64), rtol, key)
-    a = {k: v for k, v in runs[1].items() if k not in ("dW", "W", "m", "v", "bias")}
-    b = {k: v for k, v in runs[0].items() if k not in ("dW", "W", "m", "v", "bias")}
-    _compare(a, b, False, w.value)
-    np.testing.assert_array_equal(runs[1]["I"], runs[0]["I"])
+    _compare(runs[1], runs[0], True, w.value)
 
 
 # the fused step with SET runs on the fan-in 32 path (one batch pass, several)
@@ -168,3 +164,114 @@ def test_idx16_validate_indices():
     bad = layer.validate_indices()
     torch.cuda.synchronize()
     assert int(bad.cpu().numpy()[0]) == 1
+
+
+# ---------------------------------------------------------------- against the oracle
+
+def _u16_indices(layer):
+    return layer.I.cpu().numpy().view(np.uint16).astype(np.int32)
+
+
+@pytest.mark.parametrize("name", ["c4s", "mx200", "w1024", "mx320", "c1", "k7"])
+@pytest.mark.parametrize("fused", [False, True])
+def test_idx16_step_against_oracle(name, fused):
+    """The u16 layer's step against the oracle's forward, loss, backward and
+    Adam (the checks of the int32 layer's parity test)."""
+    import torch
+    from tests.test_gpu_layer import adam_reference, check_step_result
+    w, exact, inp, bias, m0, v0 = _state(name)
+    s, t, lr, wd = 1.0 / w.B, 3, 1e-2, 1e-4
+    r, Wn, mn, vn, bn, _, _ = adam_reference(w, inp, bias, s, t=t, lr=lr, wd=wd, m0=m0.astype(np.float64),
+                                             v0=v0.astype(np.float64))
+    note("idx16 %s step %s vs oracle" % ("fused" if fused else "unfused", name))
+    layer = _layer(inp, w, bias, True, m0, v0)
+    X, off, lab = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
+    if fused:
+        loss, dX = layer.train_step(X, off, lab, t=t, s=s, lr=lr, wd=wd)
+    else:
+        loss = torch.empty(1, device="cuda:0")
+        dX = layer.backward(X, off, lab, s=s, loss_out=loss)
+        layer.adam_step(t, lr=lr, wd=wd)
+    torch.cuda.synchronize()
+    check_step_result(w, inp, layer, loss, dX, r, Wn, mn, vn, bn, t, lr, fused)
+    np.testing.assert_array_equal(_u16_indices(layer), inp.I)
+
+
+@pytest.mark.parametrize("name,mode", [("c4s", "fraction"), ("c4s", "threshold"), ("w1024", "fraction"),
+                                       ("c1", "fraction"), ("c1", "threshold"), ("k7", "fraction")])
+def test_idx16_set_against_oracle(name, mode):
+    """SET on the u16 layer: indices, masks, W, m, v bit for bit against the
+    oracle on the same state."""
+    import torch
+    w, exact, inp, bias, m0, v0 = _state(name)
+    seed, rnd = 0x1616, 2
+    note("idx16 SET %s %s vs oracle" % (name, mode))
+    layer = _layer(inp, w, bias, True, m0, v0)
+    if mode == "fraction":
+        mask, ex = layer.set_update(0.25, seed, rnd)
+    else:
+        mask, ex = layer.set_update_threshold(0.05, seed, rnd)
+    torch.cuda.synchronize()
+    Wb = inp.W.view(np.uint32) if w.value == "f32" else inp.W
+    if mode == "fraction":
+        Wr, Ir, mr, vr, maskr, exr = oracle.set_update(Wb, inp.I, m0, v0, w.d, 0.25, seed, rnd)
+    else:
+        Wr, Ir, mr, vr, maskr, exr = oracle.set_update_threshold(Wb, inp.I, m0, v0, w.d, float(np.float32(0.05)),
+                                                                 seed, rnd)
+    assert int(ex.cpu().numpy()[0]) == exr
+    np.testing.assert_array_equal(_u16_indices(layer), Ir)
+    np.testing.assert_array_equal(mask.cpu().numpy(), maskr)
+    Wg = from_torch_bits(layer.W, w.value)
+    np.testing.assert_array_equal(Wg.view(np.uint32) if w.value == "f32" else Wg, Wr)
+    np.testing.assert_array_equal(layer.m.cpu().numpy().view(np.uint32), mr.view(np.uint32))
+    np.testing.assert_array_equal(layer.v.cpu().numpy().view(np.uint32), vr.view(np.uint32))
+    assert maskr.sum() > 0
+
+
+@pytest.mark.parametrize("name", ["c4s", "mx200"])
+def test_idx16_fused_step_set_against_oracle(name):
+    """The one-call step with SET on the u16 layer: the oracle's SET on the
+    GPU's exact pre-SET state (the u16 layer's plain step on a copy), bit for
+    bit on every row."""
+    import torch
+    w, exact, inp, bias, m0, v0 = _state(name)
+    X, off, lab = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
+    note("idx16 step+SET %s vs oracle: plain step on a copy" % name)
+    twin = _layer(inp, w, bias, True, m0, v0)
+    twin.train_step(X, off, lab, t=1, lr=1e-2)
+    torch.cuda.synchronize()
+    pre = (from_torch_bits(twin.W, w.value).copy(), _u16_indices(twin), twin.m.cpu().numpy().copy(),
+           twin.v.cpu().numpy().copy())
+    del twin
+    note("idx16 step+SET %s vs oracle: one call" % name)
+    layer = _layer(inp, w, bias, True, m0, v0)
+    loss, dX, mask, ex = layer.train_step_set(X, off, lab, t=1, frac=0.1, seed=99, set_round=3, lr=1e-2)
+    torch.cuda.synchronize()
+    Wr, Ir, mr, vr, maskr, exr = oracle.set_update(*pre, w.d, 0.1, 99, 3)
+    assert int(ex.cpu().numpy()[0]) == exr == 0
+    np.testing.assert_array_equal(_u16_indices(layer), Ir)
+    np.testing.assert_array_equal(mask.cpu().numpy(), maskr)
+    np.testing.assert_array_equal(from_torch_bits(layer.W, w.value), Wr)
+    np.testing.assert_array_equal(layer.m.cpu().numpy().view(np.uint32), mr.view(np.uint32))
+    np.testing.assert_array_equal(layer.v.cpu().numpy().view(np.uint32), vr.view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["c4s", "w1024", "k7"])
+def test_idx16_topk_against_oracle(name):
+    """Top-k inference on the u16 layer against the oracle's scores (the
+    validity checks of the int32 layer's top-k test)."""
+    import torch
+    from tests.test_gpu_topk import check_topk
+    w, exact, inp, bias, m0, v0 = _state(name)
+    K = 5
+    Xv, Wv = values_f64(inp.X, w.value), values_f64(inp.W, w.value)
+    z = oracle.forward(Xv, Wv, inp.I, bias.astype(np.float64))
+    tol = 1e-5 * oracle.forward(np.abs(Xv), np.abs(Wv), inp.I, np.abs(bias).astype(np.float64)) + 1e-30
+    note("idx16 topk %s vs oracle" % name)
+    layer = _layer(inp, w, bias, True, m0, v0)
+    X, off, lab = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
+    top, sc, p = layer.infer_topk(X, K, off, lab)
+    torch.cuda.synchronize()
+    top = top.cpu().numpy()
+    check_topk(top, sc.cpu().numpy().astype(np.float64), z, tol, K)
+    np.testing.assert_allclose(p.cpu().numpy(), oracle.precision_at_k(top, inp.off, inp.lab), rtol=1e-6, atol=1e-7)

@@ -171,39 +171,46 @@ def test_unfused_step_and_fused_step(torch_cuda, name, wd):
             dX = layer.backward(X, off, lab, s=s, loss_out=loss)
             layer.adam_step(t, lr=lr, wd=wd)
         torch.cuda.synchronize()
-        Wbits = from_torch_bits(layer.W, w.value)
-        Wg = values_f64(Wbits, w.value)
-        W0 = values_f64(inp.W, w.value)
-        if w.value == "f32":
-            assert_close(Wg - W0, Wn - W0, rtol, "W update")
-        else:
-            # the stored weight is the oracle's update rounded to bf16; fp32 and
-            # float64 results may straddle a rounding boundary in rare slots
-            Wref = values_f64(oracle.round_bf16(Wn), "bf16")
-            diff = np.abs(Wg - Wref)
-            # one bf16 ulp of the larger neighbour, plus an absolute floor for
-            # weights that an update drives to ~0: there the fp32 update itself
-            # (dW summed in fp32, then m/sqrt(v)) differs from float64 by up to
-            # ~1e-5 of its size, which is ~lr.
-            allow = 2.0 ** -7 * np.maximum(np.abs(Wg), np.abs(Wref)) + 1e-5 * lr
-            if fused:
-                allow = allow + 1.5 * fused_update_bound(r, inp, w, mn, vn, t, lr)
-            bad = diff > allow
-            if bad.any():
-                rows = ["slot      gpu          ref(bf16)    oracle       start        allow"]
-                for (li, ji) in np.argwhere(bad)[:8]:
-                    rows.append("%5d,%-3d %+.6e %+.6e %+.6e %+.6e %.2e" % (
-                        li, ji, Wg[li, ji], Wref[li, ji], Wn[li, ji], W0[li, ji], allow[li, ji]))
-                rows.append("count %d of %d" % (bad.sum(), bad.size))
-                raise AssertionError("W off by more than 1 ulp\n" + "\n".join(rows))
-            if not fused:
-                assert (diff > 0).mean() < 1e-3, (diff > 0).mean()
-        assert_close(Wg, Wn, rtol, "W")
-        assert_close(layer.m.cpu().numpy(), mn, rtol, "m")
-        assert_close(layer.v.cpu().numpy(), vn, rtol, "v")
-        assert_close(layer.bias.cpu().numpy(), bn, rtol, "bias")
-        assert_close(dX.cpu().numpy(), r["dX"], rtol, "dX")
-        assert_close(loss.cpu().numpy()[0], r["loss"], rtol, "loss")
+        check_step_result(w, inp, layer, loss, dX, r, Wn, mn, vn, bn, t, lr, fused)
+
+
+def check_step_result(w, inp, layer, loss, dX, r, Wn, mn, vn, bn, t, lr, fused):
+    """A training step's W, m, v, bias, dX and loss against the oracle's step
+    (r: loss_and_grads; Wn, mn, vn, bn: the oracle's Adam results)."""
+    rtol = rtol_for(w.value)
+    Wbits = from_torch_bits(layer.W, w.value)
+    Wg = values_f64(Wbits, w.value)
+    W0 = values_f64(inp.W, w.value)
+    if w.value == "f32":
+        assert_close(Wg - W0, Wn - W0, rtol, "W update")
+    else:
+        # the stored weight is the oracle's update rounded to bf16; fp32 and
+        # float64 results may straddle a rounding boundary in rare slots
+        Wref = values_f64(oracle.round_bf16(Wn), "bf16")
+        diff = np.abs(Wg - Wref)
+        # one bf16 ulp of the larger neighbour, plus an absolute floor for
+        # weights that an update drives to ~0: there the fp32 update itself
+        # (dW summed in fp32, then m/sqrt(v)) differs from float64 by up to
+        # ~1e-5 of its size, which is ~lr.
+        allow = 2.0 ** -7 * np.maximum(np.abs(Wg), np.abs(Wref)) + 1e-5 * lr
+        if fused:
+            allow = allow + 1.5 * fused_update_bound(r, inp, w, mn, vn, t, lr)
+        bad = diff > allow
+        if bad.any():
+            rows = ["slot      gpu          ref(bf16)    oracle       start        allow"]
+            for (li, ji) in np.argwhere(bad)[:8]:
+                rows.append("%5d,%-3d %+.6e %+.6e %+.6e %+.6e %.2e" % (
+                    li, ji, Wg[li, ji], Wref[li, ji], Wn[li, ji], W0[li, ji], allow[li, ji]))
+            rows.append("count %d of %d" % (bad.sum(), bad.size))
+            raise AssertionError("W off by more than 1 ulp\n" + "\n".join(rows))
+        if not fused:
+            assert (diff > 0).mean() < 1e-3, (diff > 0).mean()
+    assert_close(Wg, Wn, rtol, "W")
+    assert_close(layer.m.cpu().numpy(), mn, rtol, "m")
+    assert_close(layer.v.cpu().numpy(), vn, rtol, "v")
+    assert_close(layer.bias.cpu().numpy(), bn, rtol, "bias")
+    assert_close(dX.cpu().numpy(), r["dX"], rtol, "dX")
+    assert_close(loss.cpu().numpy()[0], r["loss"], rtol, "loss")
 
 
 def test_edge_targets(torch_cuda):
@@ -246,23 +253,32 @@ def test_accumulate_flags(torch_cuda):
     assert_close(loss.cpu().numpy()[0], ref["loss"] + 2.0, 2e-2, "loss accumulated")
 
 
-def test_run_to_run_reproducible_loss_and_weights(torch_cuda):
+@pytest.mark.parametrize("name", ["c2s", "c4s", "w1024", "c1", "mx320", "k100"])
+def test_run_to_run_reproducible_loss_and_weights(torch_cuda, name):
+    """Every sum is formed in a fixed order on every path (the fast paths'
+    matrix-core dX and fixed reduction trees; the general path's dX adds taken
+    wave by wave), so two runs give the same bits: the fused step (loss, W, m,
+    dX) and the unfused backward (dW, dX)."""
     torch = torch_cuda
-    w, inp, bias = case_inputs("c2s", seed=5)
+    w, inp, bias = case_inputs(name, seed=5)
     outs = []
     for rep in range(2):
-        note("reproducibility rep %d" % rep)
+        note("reproducibility %s rep %d" % (name, rep))
         layer = make_gpu_layer(inp, w, bias_values=bias)
         X, off, lab = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
         loss, dX = layer.train_step(X, off, lab, t=1)
         torch.cuda.synchronize()
-        outs.append((loss.cpu().numpy().copy(), from_torch_bits(layer.W, w.value).copy(),
-                     layer.m.cpu().numpy().copy(), dX.cpu().numpy().copy()))
-    # the loss and every per-row result are computed in a fixed order
-    assert np.array_equal(outs[0][0], outs[1][0])
-    assert np.array_equal(outs[0][1], outs[1][1])
-    assert np.array_equal(outs[0][2], outs[1][2])
-    assert_close(outs[0][3], outs[1][3], 1e-5, "dX between runs")
+        unf = make_gpu_layer(inp, w, bias_values=bias)
+        dXu = unf.backward(X, off, lab)
+        torch.cuda.synchronize()
+        outs.append([loss.cpu().numpy().copy(), from_torch_bits(layer.W, w.value).copy(),
+                     layer.m.cpu().numpy().copy(), dX.cpu().numpy().copy(), unf.dW.cpu().numpy().copy(),
+                     dXu.cpu().numpy().copy()])
+    for i, what in enumerate(("loss", "W", "m", "dX", "dW (unfused)", "dX (unfused)")):
+        a, b = np.asarray(outs[0][i]), np.asarray(outs[1][i])
+        if a.dtype.kind == "f":
+            a, b = a.view(np.uint32), b.view(np.uint32)
+        assert np.array_equal(a, b), what
 
 
 def test_errors_are_reported_before_launch(torch_cuda):
@@ -283,3 +299,66 @@ def test_errors_are_reported_before_launch(torch_cuda):
         layer.forward_loss(Xbig, offbig, lab[:0])
     with pytest.raises(FfslError):
         layer.adam_step(0)
+
+
+def test_workspace_carries_only_what_the_path_uses(torch_cuda):
+    """The dW carry and the fast paths' batch buffers are reserved only for
+    shapes the fused fast paths take (bf16, fan-in 32 up to width 768 or fan-in
+    64 up to 2048): an fp32 layer of the same shape, or a bf16 layer at a width
+    off the fast path, needs only the partial sums."""
+    from paper_2411_03171_amd import ffsl
+    lib = ffsl.load()
+    L, B, nnz = 3_145_728, 128, 1024
+    bf16 = lib.ffsl_workspace_bytes_ex(L, 768, 32, ffsl.FFSL_BF16, B, nnz)
+    f32 = lib.ffsl_workspace_bytes_ex(L, 768, 32, ffsl.FFSL_F32, B, nnz)
+    off_path = lib.ffsl_workspace_bytes_ex(L, 320, 32, ffsl.FFSL_BF16, B, nnz)
+    carry = 4 * (L * 32 + L)
+    assert bf16 >= f32 + carry
+    assert off_path < f32 and f32 < carry
+    # the call without a type is the bf16 layout (an upper bound for both)
+    assert lib.ffsl_workspace_bytes(L, 768, 32, B, nnz) == bf16
+    assert lib.ffsl_workspace_bytes_ex(L, 768, 32, 9, B, nnz) == 0
+
+
+@pytest.mark.parametrize("name", ["c4s", "mx200", "w1024", "c1", "mx320"])
+def test_nan_in_x_gives_nan_loss_and_a_normal_return(torch_cuda, name):
+    """A NaN in one input column of one sample: the call returns normally, the
+    loss is NaN (as the oracle's), the rows that gather that column get NaN
+    weights, and the clean samples' dX and the other rows' weights still match
+    the oracle.  A clean step afterwards runs as usual."""
+    torch = torch_cuda
+    w, inp, bias = case_inputs(name, seed=6)
+    Xbad = inp.X.copy()
+    b_nan, col = 1, 5
+    if w.value == "f32":
+        Xbad[b_nan, col] = np.nan
+    else:
+        Xbad[b_nan, col] = 0x7FC0
+    inp_bad = synth.dataclasses.replace(inp, X=Xbad)
+    s, t, lr = 1.0 / w.B, 1, 1e-3
+    r, Wn, mn, vn, bn, _, _ = adam_reference(w, inp_bad, bias, s, t=t, lr=lr)
+    assert np.isnan(r["loss"])
+    note("NaN in X %s" % name)
+    layer = make_gpu_layer(inp_bad, w, bias_values=bias)
+    X, off, lab = batch_to_gpu(Xbad, inp.off, inp.lab, w.value)
+    loss, dX = layer.train_step(X, off, lab, t=t, s=s, lr=lr)
+    torch.cuda.synchronize()
+    assert np.isnan(float(loss.cpu()[0]))
+    touched = np.any(inp.I == col, axis=1)
+    assert touched.any() and not touched.all()
+    Wg = values_f64(from_torch_bits(layer.W, w.value), w.value)
+    assert np.isnan(Wg[touched]).all()
+    assert np.isfinite(Wg[~touched]).all()
+    rtol = rtol_for(w.value)
+    assert_close(Wg[~touched], Wn[~touched], rtol, "W of the rows that do not gather the NaN column")
+    clean = np.arange(w.B) != b_nan
+    dXg = dX.cpu().numpy()
+    assert np.isfinite(dXg[clean]).all()
+    assert_close(dXg[clean], r["dX"][clean], rtol, "dX of the clean samples")
+    # the device and the library carry on
+    note("NaN in X %s: a clean step afterwards" % name)
+    layer2 = make_gpu_layer(inp, w, bias_values=bias)
+    X2, off2, lab2 = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
+    loss2, _ = layer2.train_step(X2, off2, lab2, t=1, s=s)
+    torch.cuda.synchronize()
+    assert np.isfinite(float(loss2.cpu()[0]))

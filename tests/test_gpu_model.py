@@ -147,15 +147,11 @@ def test_model_aux_head_step(torch_cuda, epoch, set_step):
     r = _sparse_ref(inp, w, X, bias, inp.off, inp.lab, m0, v0, t, lr, wd)
     loss_ref, dX_ref = r["loss"], r["dX"].copy()
     if wgt > 0:
-        a = oracle.aux_bce(X, _f64(Wa), ca.astype(np.float64), inp.off, inp.lab, wgt / w.B)
+        a = oracle.aux_bce(X, _f64(Wa), ca.astype(np.float64), inp.off, inp.lab, wgt / w.B, w.L)
         loss_ref += a["loss"]
         dX_ref += a["dXa"]
         Wan, mAn, vAn = oracle.adam(_f64(Wa), mA0, vA0, a["dWa"], t, lr=lr_a)
         can, mcn, vcn = oracle.adam(ca.astype(np.float64), mc0, vc0, a["dca"], t, lr=lr_a)
-    if set_step:
-        Wb = oracle.round_bf16(r["W"])
-        Wset, Iset, mset, vset, mask_ref, _ = oracle.set_update(Wb, inp.I, r["m"], r["v"], w.d, 0.25, 77,
-                                                                schedule.set_round(t, interval))
 
     dev = "cuda:0"
     note("model step: aux head epoch=%g set=%s B=%d d=%d C=%d L=%d" % (epoch, set_step, w.B, w.d, C, w.L))
@@ -169,6 +165,18 @@ def test_model_aux_head_step(torch_cuda, epoch, set_step):
     for x, y in ((model.mWa, mA0), (model.vWa, vA0), (model.mca, mc0), (model.vca, vc0)):
         x.copy_(torch.from_numpy(y))
     Xt, offt, labt = batch_to_gpu(inp.X, inp.off, inp.lab, "bf16")
+    pre = None
+    if set_step:
+        # the sparse layer's pre-SET state: the plain step on a copy with the
+        # same state and arguments
+        twin = make_gpu_layer(inp, w, bias_values=bias, unfused=False)
+        twin.m.copy_(torch.from_numpy(m0))
+        twin.v.copy_(torch.from_numpy(v0))
+        twin.train_step(Xt, offt, labt, t, lr=lr, wd=wd)
+        torch.cuda.synchronize()
+        pre = (from_torch_bits(twin.W, "bf16").copy(), twin.I.cpu().numpy().copy(), twin.m.cpu().numpy().copy(),
+               twin.v.cpu().numpy().copy())
+        del twin
     loss, dX, mask = model.train_step(Xt, offt, labt, t, epoch=epoch)
     torch.cuda.synchronize()
     assert_close(np.array([float(loss.cpu()[0])]), np.array([loss_ref]), RTOL_BF16, "loss")
@@ -182,15 +190,18 @@ def test_model_aux_head_step(torch_cuda, epoch, set_step):
         np.testing.assert_array_equal(from_torch_bits(model.Wa, "bf16"), Wa)
         np.testing.assert_array_equal(model.mWa.cpu().numpy(), mA0)
     if set_step:
-        # the topology update follows the step: compare what is decided by the
-        # draw stream and the pruned magnitudes (the bf16 weights can differ by
-        # one rounding from the oracle's, so only rows whose pruned set is the
-        # same are compared index for index)
+        # the topology update follows the step: the oracle's SET on the GPU's
+        # exact pre-SET state, bit for bit on every row
         assert mask is not None
+        Wset, Iset, mset, vset, mask_ref, ex = oracle.set_update(*pre, w.d, 0.25, 77,
+                                                                 schedule.set_round(t, interval))
+        assert ex == 0
         Ig = layer.I.cpu().numpy()
-        same = np.all(mask.cpu().numpy() == mask_ref, axis=1)
-        assert same.mean() > 0.95, same.mean()
-        np.testing.assert_array_equal(Ig[same], Iset[same])
+        np.testing.assert_array_equal(Ig, Iset)
+        np.testing.assert_array_equal(mask.cpu().numpy(), mask_ref)
+        np.testing.assert_array_equal(from_torch_bits(layer.W, "bf16"), Wset)
+        np.testing.assert_array_equal(layer.m.cpu().numpy().view(np.uint32), mset.view(np.uint32))
+        np.testing.assert_array_equal(layer.v.cpu().numpy().view(np.uint32), vset.view(np.uint32))
         assert np.all(np.diff(np.sort(Ig, axis=1), axis=1) > 0)
     else:
         assert mask is None

@@ -85,10 +85,8 @@ def test_fused_equals_step_then_set(name, frac):
     ref = _run(w, inp, bias, m0, v0, False, frac, wd)
     note("train+SET %s frac=%g: one call" % (name, frac))
     got = _run(w, inp, bias, m0, v0, True, frac, wd)
-    # the general path (width 320) sums dX with LDS float atomics, whose order
-    # changes from run to run: there dX and the loss agree to the bf16 bar;
-    # everything else, and both fast paths' dX and loss, bit for bit
-    exact = ("W", "I", "m", "v", "bias", "mask") + (("dX",) if name != "mx320" else ())
+    # every path forms its sums in a fixed order: everything bit for bit
+    exact = ("W", "I", "m", "v", "bias", "mask", "dX")
     for key in exact:
         a, b = got[key], ref[key]
         if a.dtype.kind == "f":
@@ -96,54 +94,61 @@ def test_fused_equals_step_then_set(name, frac):
         bad = np.argwhere(a != b)
         assert len(bad) == 0, "%s differs at %d entries, first %s" % (key, len(bad), bad[:4].tolist())
     assert got["ex"] == ref["ex"]
-    if name == "mx320":
-        assert_close(got["dX"], ref["dX"].astype(np.float64), RTOL_BF16, "dX")
-        assert_close(np.array([got["loss"]]), np.array([ref["loss"]]), RTOL_BF16, "loss")
-    else:
-        assert np.float32(got["loss"]).view(np.uint32) == np.float32(ref["loss"]).view(np.uint32)
+    assert np.float32(got["loss"]).view(np.uint32) == np.float32(ref["loss"]).view(np.uint32)
     # no row runs out of attempts at these widths: every row regrows n slots
     n = int(np.floor(frac * inp.I.shape[1] + 1e-9))
     assert got["ex"] == 0
     assert (got["mask"].sum(axis=1) == n).all()
 
 
-def test_fused_against_oracle():
-    """The one-call step against the oracle's train step followed by its SET.
-    The oracle prunes by the float64 update rounded to bf16; where a weight's
-    rounding differs by an ulp, a row's pruned set can differ, so rows are
-    compared where the pruned sets agree (nearly all) and every row must hold
-    k distinct columns with the regrown ones absent before the step."""
+def _step_only(w, inp, bias, m0, v0, wd, t, lr):
+    """The plain training step (no SET) from the same state: the pre-SET state
+    of the one-call step."""
+    import torch
+    layer = make_gpu_layer(inp, w, bias_values=bias, unfused=False)
+    layer.m.copy_(torch.from_numpy(m0))
+    layer.v.copy_(torch.from_numpy(v0))
+    X, off, lab = batch_to_gpu(inp.X, inp.off, inp.lab, w.value)
+    layer.train_step(X, off, lab, t=t, s=1.0 / w.B, lr=lr, wd=wd)
+    torch.cuda.synchronize()
+    return (from_torch_bits(layer.W, w.value).copy(), layer.I.cpu().numpy().copy(), layer.m.cpu().numpy().copy(),
+            layer.v.cpu().numpy().copy())
+
+
+@pytest.mark.parametrize("name,frac,wd", [("c4s", 0.1, 0.0), ("mx200", 0.25, 1e-4), ("b1", 0.1, 0.0)])
+def test_fused_against_oracle(name, frac, wd):
+    """The one-call step against the oracle.  The step's loss and dX against the
+    oracle's step within the bf16 bar; SET bit for bit on every row: the
+    oracle's SET runs on the GPU's exact pre-SET state (W bits, I, m, v of the
+    plain step on an identical copy), and the one-call result must equal it in
+    W, I, m, v and the mask."""
     import torch
     assert torch.cuda.is_available(), "GPU tests need a GPU"
-    w, inp, bias, m0, v0 = _state("c4s", seed=4)
-    frac, seed, rnd, t, lr = 0.1, 123, 2, 3, 1e-2
-    note("train+SET c4s vs oracle")
-    got = _run(w, inp, bias, m0, v0, True, frac, 0.0, t=t, lr=lr, seed=seed, rnd=rnd)
+    w, inp, bias, m0, v0 = _state(name, seed=4)
+    seed, rnd, t, lr = 123, 2, 3, 1e-2
+    note("train+SET %s vs oracle: one call" % name)
+    got = _run(w, inp, bias, m0, v0, True, frac, wd, t=t, lr=lr, seed=seed, rnd=rnd)
+    note("train+SET %s vs oracle: the plain step on a copy" % name)
+    Wp, Ip, mp, vp = _step_only(w, inp, bias, m0, v0, wd, t, lr)
+    Wr, Ir, mr, vr, maskr, exr = oracle.set_update(Wp, Ip, mp, vp, w.d, frac, seed, rnd)
+    assert exr == 0 and got["ex"] == 0
+    np.testing.assert_array_equal(got["I"], Ir)
+    np.testing.assert_array_equal(got["mask"], maskr)
+    np.testing.assert_array_equal(got["W"], Wr)
+    np.testing.assert_array_equal(got["m"].view(np.uint32), mr.view(np.uint32))
+    np.testing.assert_array_equal(got["v"].view(np.uint32), vr.view(np.uint32))
+    n = oracle.set_prune_count(w.k, frac)
+    assert (maskr.sum(axis=1) == n).all()
+    # the step itself against the oracle's step
     X = values_f64(inp.X, "bf16")
     W = values_f64(inp.W, "bf16")
     r = oracle.train_step(X, W, inp.I, bias.astype(np.float64), m0.astype(np.float64), v0.astype(np.float64),
                           np.zeros(len(bias)), np.zeros(len(bias)), inp.off, inp.lab, 1.0 / w.B, t=t, lr=lr,
-                          w_bf16=True)
-    Wb, I2, m2, v2, mask2, ex2 = oracle.set_update(oracle.round_bf16(r["W"]), inp.I, r["m"].astype(np.float32),
-                                                   r["v"].astype(np.float32), w.d, frac, seed, rnd)
-    assert ex2 == 0 and got["ex"] == 0
-    same = np.all(got["mask"] == mask2, axis=1)
-    assert same.mean() > 0.99, same.mean()
-    assert (got["I"][same] == I2[same]).all()
-    # weights to the bf16 bar (the fp32 update and the float64 one can round
-    # to neighbouring bf16 values); regrown slots are exactly zero on both sides
-    assert_close(values_f64(got["W"][same], "bf16"), values_f64(Wb[same], "bf16"), RTOL_BF16, "W")
-    assert_close(got["m"][same], m2[same].astype(np.float64), RTOL_BF16, "m")
-    assert_close(got["v"][same], v2[same].astype(np.float64), RTOL_BF16, "v")
+                          wd=wd, w_bf16=True)
     assert_close(np.array([got["loss"]]), np.array([r["loss"]]), RTOL_BF16, "loss")
     assert_close(got["dX"], r["dX"], RTOL_BF16, "dX")
-    # every row: k distinct columns in range, regrown columns new to the row
-    Ig = got["I"]
-    k = Ig.shape[1]
-    assert all(len(set(row.tolist())) == k for row in Ig)
-    assert Ig.min() >= 0 and Ig.max() < w.d
-    for l in np.nonzero(got["mask"].any(axis=1))[0][:200]:
-        regrown = Ig[l][got["mask"][l] == 1]
+    assert_close(got["m"][maskr == 0], r["m"][maskr == 0], RTOL_BF16, "m of the survivors")
+    # regrown columns are new to the row
+    for l in np.nonzero(maskr.any(axis=1))[0][:200]:
+        regrown = Ir[l][maskr[l] == 1]
         assert not (set(regrown.tolist()) & set(inp.I[l].tolist()))
-        assert (got["W"][l][got["mask"][l] == 1] == 0).all()
-        assert (got["m"][l][got["mask"][l] == 1] == 0).all()

@@ -41,7 +41,7 @@ def test_aux_head_matches_torch(oracle):
     off = np.array([0, 2, 3, 6, 7])
     lab = np.array([3, 8, 22, 0, 5, 10, 4], dtype=np.int32)   # 0,5,10 share cluster 0
     s = 1 / B
-    r = oracle.aux_bce(X, Wa, ca, off, lab, s)
+    r = oracle.aux_bce(X, Wa, ca, off, lab, s, L)
     ya = np.zeros((B, C))
     for b in range(B):
         for l in lab[off[b]:off[b + 1]]:
@@ -57,3 +57,49 @@ def test_aux_head_matches_torch(oracle):
     np.testing.assert_allclose(r["dWa"], Wt.grad.numpy(), rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(r["dca"], ct.grad.numpy(), rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(r["dXa"], Xt.grad.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_label_range_is_the_same_for_both_heads(oracle):
+    """A label outside [0, L) is not a label of the layer: the sparse head's
+    targets and the auxiliary head's cluster targets both ignore it, so a batch
+    with such labels gives the results of the batch without them.  Pinned
+    against a hand-built cluster multi-hot and torch's BCE, and by the sparse
+    targets of both batches."""
+    rng = np.random.default_rng(2)
+    B, d, C, L = 3, 5, 4, 10
+    X = rng.standard_normal((B, d))
+    Wa = rng.standard_normal((d, C)) * 0.3
+    ca = rng.standard_normal(C)
+    # out of range: -1, -7 (negative), 10 = L, 11 and 14 (clusters 2, 3, 2 if
+    # they were taken, none of them a cluster the sample already has);
+    # in range: 2, 9, 4
+    off = np.array([0, 3, 5, 8])
+    lab = np.array([2, 11, -1, 9, 14, 4, -7, 10], dtype=np.int32)
+    keep = (lab >= 0) & (lab < L)
+    off_in = np.concatenate([[0], np.cumsum([keep[off[b]:off[b + 1]].sum() for b in range(B)])])
+    lab_in = lab[keep]
+    s = 0.5
+    r = oracle.aux_bce(X, Wa, ca, off, lab, s, L)
+    r_in = oracle.aux_bce(X, Wa, ca, off_in, lab_in, s, L)
+    for key in ("loss", "Za", "dWa", "dca", "dXa"):
+        np.testing.assert_array_equal(r[key], r_in[key])
+    ya = np.zeros((B, C))
+    ya[0, 2 % C] = 1
+    ya[1, 9 % C] = 1
+    ya[2, 4 % C] = 1
+    loss = torch.nn.functional.binary_cross_entropy_with_logits(
+        torch.tensor(X @ Wa + ca), torch.tensor(ya), reduction="sum") * s
+    np.testing.assert_allclose(r["loss"], loss.item(), rtol=1e-13)
+    # the sparse head's targets drop the same labels
+    y = oracle.targets_dense(B, L, off, lab)
+    y_in = oracle.targets_dense(B, L, off_in, lab_in)
+    np.testing.assert_array_equal(y, y_in)
+    assert y.sum() == 3
+    # the other reading (labels >= L mapped to l mod C) gives other targets,
+    # so the pin tells the two apart
+    ya_other = ya.copy()
+    ya_other[0, 11 % C] = ya_other[1, 14 % C] = ya_other[2, 10 % C] = 1
+    assert not np.array_equal(ya, ya_other)
+    loss_other = torch.nn.functional.binary_cross_entropy_with_logits(
+        torch.tensor(X @ Wa + ca), torch.tensor(ya_other), reduction="sum") * s
+    assert abs(r["loss"] - loss_other.item()) > 1e-3
