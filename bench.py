@@ -290,9 +290,39 @@ def time_c2_run(torch, ffsl, synth, dev, seed):
     return out
 
 
-def cpu_baseline(w, inp, target_s=12.0):
-    """The oracle (float64, single thread) on the first L' label rows of the
-    same workload: one fused step (forward, BCE, backward, Adam)."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def cpu_threads():
+    """Threads for the multi-core leg: the CPU share this process may use
+    (affinity), at most 16 (one GPU's share of the box)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, os.cpu_count() or 1, 16))
+
+
+def cpu_baseline(w, inp, target_s=5.0, set_target_s=2.0):
+    """The oracle (float64, plain loops, unchanged) on bounded samples of the
+    same workload, three legs:
+      - single thread: one fused step (forward, BCE, dW, dbias, dX, Adam) on a
+        block of label rows;
+      - multi-core: the same call on T disjoint row blocks at once, one thread
+        per block (the oracle's C calls release the GIL; the blocks' dX
+        partials would add up to the step's dX);
+      - SET: one prune-and-regrow round on a block of rows.
+    Each block is calibrated to about target_s seconds of work."""
+    import concurrent.futures as cf
+
     import numpy as np
 
     import oracle
@@ -303,37 +333,71 @@ def cpu_baseline(w, inp, target_s=12.0):
     W = synth.bf16_bits_to_f32(inp.W).astype(np.float64) if w.value == "bf16" else \
         inp.W.astype(np.float64)
 
-    def run(Ls):
-        keep = np.zeros(len(inp.lab), dtype=bool)
+    def targets(r0, Ls):
         off = np.zeros(w.B + 1, dtype=np.int64)
         labs = []
         for b in range(w.B):
             seg = inp.lab[inp.off[b]:inp.off[b + 1]]
-            seg = seg[seg < Ls]
+            seg = seg[(seg >= r0) & (seg < r0 + Ls)] - r0
             labs.append(seg)
             off[b + 1] = off[b] + len(seg)
-        lab = np.concatenate(labs).astype(np.int32)
+        return off, np.concatenate(labs).astype(np.int32)
+
+    def step(r0, Ls):
+        off, lab = targets(r0, Ls)
+        sl = slice(r0, r0 + Ls)
         t0 = time.perf_counter()
-        oracle.train_step(X, W[:Ls], inp.I[:Ls], np.zeros(Ls), np.zeros((Ls, w.k)),
-                          np.zeros((Ls, w.k)), np.zeros(Ls), np.zeros(Ls), off, lab,
-                          1.0 / w.B, t=1, w_bf16=(w.value == "bf16"))
+        oracle.train_step(X, W[sl], inp.I[sl], np.zeros(Ls), np.zeros((Ls, w.k)), np.zeros((Ls, w.k)),
+                          np.zeros(Ls), np.zeros(Ls), off, lab, 1.0 / w.B, t=1, w_bf16=(w.value == "bf16"))
         return time.perf_counter() - t0
 
-    Ls = min(w.L, 32768)
-    dt = run(Ls)
-    Ls2 = int(min(w.L, max(Ls, Ls * target_s / max(dt, 1e-3))))
-    if Ls2 > Ls:
-        Ls = Ls2
-        dt = run(Ls)
+    # single thread, calibrated
+    Ls = min(w.L, 16384)
+    dt = step(0, Ls)
+    Ls = int(min(w.L, max(Ls, Ls * target_s / max(dt, 1e-3))))
+    dt = step(0, Ls)
+    single = w.B * Ls / dt
+
+    # multi-core: T blocks of Lb rows in T threads
+    T = cpu_threads()
+    Lb = max(1, min(Ls, w.L // T))
+    with cf.ThreadPoolExecutor(max_workers=T) as ex:
+        t0 = time.perf_counter()
+        list(ex.map(lambda p: step(p * Lb, Lb), range(T)))
+        dt_mc = time.perf_counter() - t0
+    multi = w.B * T * Lb / dt_mc
+
+    # SET: one round on a block of rows (fraction mode, the workload's fraction)
+    Wbits = inp.W if w.value == "bf16" else inp.W.view(np.uint32)
+    zeros = None
+
+    def set_round(Lr):
+        nonlocal zeros
+        if zeros is None or zeros.shape[0] < Lr:
+            zeros = np.zeros((Lr, w.k), dtype=np.float32)
+        t0 = time.perf_counter()
+        oracle.set_update(Wbits[:Lr], inp.I[:Lr], zeros[:Lr], zeros[:Lr], w.d, w.set_frac, 7, 0)
+        return time.perf_counter() - t0
+
+    Lr = min(w.L, 65536)
+    ds = set_round(Lr)
+    Lr = int(min(w.L, max(Lr, Lr * set_target_s / max(ds, 1e-3))))
+    ds = set_round(Lr)
     return {
-        "value": w.B * Ls / dt,
+        "value": multi,
         "unit": "sample*labels/s",
-        "cores": 1,
+        "cores": T,
         "kind": "oracle",
-        "sample": "first %d of %d label rows of the workload (same X, targets restricted to "
-                  "those rows), one fused step: forward, BCE, dW, dbias, dX, Adam; float64, "
-                  "single thread, %.1f s" % (Ls, w.L, dt),
-        "cpu": platform.processor() or platform.machine(),
+        "sample": "one fused step (forward, BCE, dW, dbias, dX, Adam; float64) of the oracle on %d disjoint "
+                  "blocks of %d label rows of the workload (same X, targets restricted to each block), one "
+                  "thread per block, %.1f s wall" % (T, Lb, dt_mc),
+        "single_thread": {"value": single, "unit": "sample*labels/s", "cores": 1,
+                          "sample": "first %d of %d label rows, %.1f s" % (Ls, w.L, dt)},
+        "set": {"rows_per_s": Lr / ds, "s_per_full_set": w.L * ds / Lr, "cores": 1,
+                "sample": "one SET round (fraction %g) on the first %d of %d rows, %.1f s" % (w.set_frac, Lr,
+                                                                                             w.L, ds)},
+        "cpu_model": cpu_model(),
+        "cpu_count": os.cpu_count(),
     }
 
 
@@ -641,8 +705,9 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, inp)
-        print("[bench] oracle: %.3e sample*labels/s (%s)" % (cpu["value"], cpu["sample"]),
-              file=sys.stderr, flush=True)
+        print("[bench] oracle: %.3e sample*labels/s on %d threads (%s); single thread %.3e; SET %.1f s per "
+              "full round" % (cpu["value"], cpu["cores"], cpu["sample"], cpu["single_thread"]["value"],
+                              cpu["set"]["s_per_full_set"]), file=sys.stderr, flush=True)
 
     value = w.B * w.L / (ms_per_step * 1e-3)
     out = {
