@@ -174,14 +174,17 @@ __device__ __forceinline__ void sort_keys512(uint32_t *tg, uint32_t k0, uint32_t
     __syncthreads();
 }
 
-// Adam with the bias corrections folded into reciprocals; fp32 throughout
+// Adam with the bias corrections folded into reciprocals; fp32 throughout.
+// Every fused multiply-add is written out, so each kernel that inlines this
+// rounds the same way (contraction left to the compiler may fuse a*b + c*d
+// either way round).
 __device__ __forceinline__ float adam_step(float p, float g, float &mm, float &vv, float b1, float b2,
                                            float inv_bc1, float inv_bc2, float lr, float eps, float decay) {
     p *= decay;
-    mm = b1 * mm + (1.f - b1) * g;
-    vv = b2 * vv + (1.f - b2) * g * g;
+    mm = fmaf(b1, mm, (1.f - b1) * g);
+    vv = fmaf(b2, vv, ((1.f - b2) * g) * g);
     const float den = __builtin_amdgcn_sqrtf(vv * inv_bc2) + eps;
-    return p - (lr * inv_bc1) * mm * __builtin_amdgcn_rcpf(den);
+    return fmaf(-((lr * inv_bc1) * mm), __builtin_amdgcn_rcpf(den), p);
 }
 
 // Regrowth draws of SET: Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)
