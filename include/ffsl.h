@@ -270,6 +270,26 @@ FFSL_API int ffsl_infer_topk(ffsl_layer *layer, const void *X, int32_t B, int32_
                     const int32_t *tgt_lab, int32_t nnz, float *p_at_k, void *workspace,
                     size_t workspace_bytes, void *stream);
 
+/* Bytes of the static scratch that ffsl_infer_topk_noalloc uses on each GPU. */
+#define FFSL_TOPK_SCRATCH_BYTES (32u << 20)
+
+/* ffsl_infer_topk for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, results and errors as ffsl_infer_topk, without the
+ * workspace: its scratch is a static device array of FFSL_TOPK_SCRATCH_BYTES
+ * (32 MiB) that each GPU the library runs on holds until the process ends.
+ * The call allocates nothing.
+ *   - A call whose ffsl_topk_workspace_bytes(layer, B, topk) exceeds
+ *     FFSL_TOPK_SCRATCH_BYTES is rejected with FFSL_EINVAL (about B * topk' <=
+ *     4000 on a 256-CU device, topk' = topk rounded up to 1, 4, 8 or 16).
+ *   - The layer's device must be the current device (else FFSL_EINVAL).
+ *   - Every call on a GPU shares that GPU's one array: calls that overlap on
+ *     one GPU (other streams, other threads) race and must be ordered.
+ *     Nothing in the array has to start at zero. */
+FFSL_API int ffsl_infer_topk_noalloc(ffsl_layer *layer, const void *X, int32_t B, int32_t topk,
+                    int32_t *top_labels, float *top_scores, const int32_t *tgt_off,
+                    const int32_t *tgt_lab, int32_t nnz, float *p_at_k, void *stream);
+
 /* SET in threshold mode (the appendix's table of DST settings: prune mode
  * "threshold" with a rewire threshold of 0.05 or 0.01): in every row, each
  * slot with |W| < tau is pruned (compared as real numbers; a NaN weight is

@@ -441,6 +441,40 @@ int ffsl_infer_topk(ffsl_layer *layer, const void *X, int32_t B, int32_t topk, i
                        static_cast<char *>(workspace), p, static_cast<hipStream_t>(stream));
 }
 
+int ffsl_infer_topk_noalloc(ffsl_layer *layer, const void *X, int32_t B, int32_t topk, int32_t *top_labels,
+                            float *top_scores, const int32_t *tgt_off, const int32_t *tgt_lab, int32_t nnz,
+                            float *p_at_k, void *stream) {
+    g_err.clear();
+    if (!layer) return fail(FFSL_EINVAL, "layer is null");
+    const Layer &ly = layer->ly;
+    if (!X) return fail(FFSL_EINVAL, "X is null");
+    if (B < 1 || B > FFSL_MAX_B) return fail(FFSL_EINVAL, "B must be in [1,%d] (got %d)", FFSL_MAX_B, B);
+    if (topk < 1 || topk > FFSL_MAX_TOPK || (int64_t)topk > ly.L)
+        return fail(FFSL_EINVAL, "topk must be in [1, min(%d, L)] (got %d)", FFSL_MAX_TOPK, topk);
+    if (!top_labels) return fail(FFSL_EINVAL, "top_labels is null");
+    if (p_at_k) {
+        if (!tgt_off) return fail(FFSL_EINVAL, "p_at_k needs tgt_off");
+        if (nnz < 0) return fail(FFSL_EINVAL, "nnz must be >= 0");
+        if (nnz > 0 && !tgt_lab) return fail(FFSL_EINVAL, "tgt_lab is null");
+    }
+    TopkPlan p{};
+    if (!topk_shape(ly, B, topk, &p))
+        return fail(FFSL_EUNSUPPORTED, "top-k inference does not support this shape (L=%lld, d=%d, %s)",
+                    (long long)ly.L, ly.d, ly.vt == FFSL_BF16 ? "bf16" : "fp32");
+    if (p.total > (size_t)FFSL_TOPK_SCRATCH_BYTES)
+        return fail(FFSL_EINVAL,
+                    "B=%d, topk=%d need %zu bytes of scratch, more than the %zu of the no-allocation call "
+                    "(use ffsl_infer_topk with a workspace, or a smaller batch)",
+                    B, topk, p.total, (size_t)FFSL_TOPK_SCRATCH_BYTES);
+    char *ws = nullptr;
+    int rc = topk_scratch(ly.device, &ws);
+    if (rc) return rc;
+    rc = topk_grid(ly, &p);
+    if (rc) return rc;
+    return launch_topk(ly, X, B, topk, top_labels, top_scores, tgt_off, tgt_lab, p_at_k, ws, p,
+                       static_cast<hipStream_t>(stream));
+}
+
 int ffsl_validate_indices(ffsl_layer *layer, int32_t *bad_rows_out, void *stream) {
     g_err.clear();
     if (!layer) return fail(FFSL_EINVAL, "layer is null");

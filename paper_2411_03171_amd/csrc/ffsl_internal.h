@@ -168,6 +168,9 @@ struct TopkPlan {
 bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p);
 // grid of the scan kernel on the current device
 int topk_grid(const Layer &ly, TopkPlan *p);
+// device address of the static scratch of the no-allocation inference call
+// on `device`, which must be the current device (FFSL_TOPK_SCRATCH_BYTES bytes)
+int topk_scratch(int device, char **ptr);
 int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_lab, float *top_sc,
                 const int32_t *off, const int32_t *lab, float *p_at_k, char *ws, const TopkPlan &p,
                 hipStream_t st);

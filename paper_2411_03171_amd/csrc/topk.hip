@@ -24,10 +24,52 @@
 // NaN scores are never selected.  A (score, label) pair is one 64-bit key
 // that orders exactly that way, so lists compare with one integer compare.
 
+#include <mutex>
+
 #include "ffsl_internal.h"
 #include "sweep_dev.h"
 
+// Scratch of the no-allocation inference call (ffsl_infer_topk_noalloc): the
+// same workspace layout as ffsl_infer_topk's, in a file-scope device array
+// that each GPU the library runs on holds until the process ends.  Host code
+// never uses this name as an address: the device address comes from
+// hipGetSymbolAddress, once per device (topk_scratch below).  Nothing in it
+// needs to start at zero: the scan writes every list the merge reads, and the
+// merge every relevance flag the P@k kernel reads.
+// The array has external linkage (and default visibility): with internal
+// linkage the device code object keeps it as a local symbol, which the
+// runtime's symbol lookup cannot find.
+__device__ __align__(256) __attribute__((visibility("default"))) unsigned char
+    ffsl_topk_scratch[FFSL_TOPK_SCRATCH_BYTES];
+
 namespace ffsl {
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[SCRATCH_MAX_DEVICES];   // device address of `scratch` per device
+}  // namespace
+
+int topk_scratch(int device, char **ptr) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (cur != device)
+        return fail(FFSL_EINVAL, "the layer lives on device %d but device %d is current", device, cur);
+    if (device < 0 || device >= SCRATCH_MAX_DEVICES)
+        return fail(FFSL_EUNSUPPORTED, "device %d: the no-allocation call supports devices 0..%d", device,
+                    SCRATCH_MAX_DEVICES - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[device]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(ffsl_topk_scratch));
+        if (e != hipSuccess || !p)
+            return fail(FFSL_EHIP, "hipGetSymbolAddress(ffsl_topk_scratch): %s", hipGetErrorString(e));
+        g_scratch[device] = p;
+    }
+    *ptr = static_cast<char *>(g_scratch[device]);
+    return FFSL_OK;
+}
 namespace {
 using namespace fdev;
 

@@ -17,6 +17,7 @@ FFSL_OK, FFSL_EINVAL, FFSL_EUNSUPPORTED, FFSL_EHIP = 0, -1, -2, -3
 FFSL_F32, FFSL_BF16 = 0, 1
 FFSL_ACCUM_DX, FFSL_ACCUM_LOSS, FFSL_LOSS_SQHINGE = 1, 2, 4
 FFSL_IDX_I32, FFSL_IDX_U16 = 0, 1
+FFSL_TOPK_SCRATCH_BYTES = 32 << 20   # static scratch of ffsl_infer_topk_noalloc per GPU
 
 # (name, restype, argtypes) for every entry point of include/ffsl.h
 _i32, _i64, _u32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
@@ -44,6 +45,7 @@ SIGNATURES = {
     "ffsl_validate_indices": (_int, [_vp, _vp, _vp]),
     "ffsl_topk_workspace_bytes": (_sz, [_vp, _i32, _i32]),
     "ffsl_infer_topk": (_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
+    "ffsl_infer_topk_noalloc": (_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "ffsl_set_timing_events": (_int, [_vp, _vp, _vp]),
     "ffsl_dense_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "ffsl_dense_gelu_fwd": (_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
