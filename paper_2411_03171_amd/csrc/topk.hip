@@ -331,6 +331,78 @@ __device__ __forceinline__ void tk_round_full(const TkRound<VT> &c, int xl, floa
     tk_fma_all<VT, SPL>(c, xa, xb, z);
 }
 
+// Stage the batch tile transposed, Xs[c*BT + b], with a zero column d and
+// zero samples past B, and clear the per-sample bounds and list bests.
+template <typename T, int BT>
+__device__ __forceinline__ void tk_stage(const TkArgs &a, int b0, int nb) {
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    const int tid = threadIdx.x, d = a.d;
+    T *Xs = reinterpret_cast<T *>(tk_smem);
+    const T *X = static_cast<const T *>(a.X) + (int64_t)b0 * d;
+    for (int b = 0; b < BT; ++b)
+        for (int c = tid; c <= d; c += TK_THREADS)
+            Xs[c * BT + b] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
+    for (int i = tid; i < BT * (1 + TK_LISTS); i += TK_THREADS)
+        reinterpret_cast<uint32_t *>(tk_smem + a.thr_off)[i] = 0u;
+    __syncthreads();
+}
+
+// Every wave turns the list bests of BT/8 samples into bounds: the K-th
+// largest of a sample's 32 list bests (K distinct labels reach it).
+template <int KP, int BT>
+__device__ __forceinline__ void tk_list_bound(const uint32_t *lmax, uint32_t *shared_thr, int K, int wave,
+                                              int lane) {
+    if (lane < BT / TK_WAVES) {
+        const int bt = wave * (BT / TK_WAVES) + lane;
+        uint32_t best[KP];
+#pragma unroll
+        for (int p = 0; p < KP; ++p) best[p] = 0u;
+        for (int i = 0; i < TK_LISTS; ++i) {
+            uint32_t v = __hip_atomic_load(lmax + bt * TK_LISTS + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+            for (int p = 0; p < KP; ++p) {
+                const uint32_t hi = max(best[p], v), lo = min(best[p], v);
+                best[p] = hi;
+                v = lo;
+            }
+        }
+        uint32_t vk = 0u;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) vk = p == K - 1 ? best[p] : vk;
+        atomicMax(shared_thr + bt, vk);
+    }
+}
+
+// The workgroup's 32 lists per sample, written to LDS as Ls[bt][list][KP],
+// merged into one per sample and written to a.part.
+template <int KP, int BT>
+__device__ __forceinline__ void tk_merge_lists(const TkArgs &a, int b0, int nb) {
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    uint64_t *Ls = reinterpret_cast<uint64_t *>(tk_smem);
+    __syncthreads();
+    constexpr int TPS = TK_THREADS / BT;    // threads per sample
+    constexpr int LPT = TK_LISTS / TPS;     // lists per thread in the first stage
+    const int tid = threadIdx.x;
+    const int bt = tid / TPS, sub = tid % TPS;
+    uint64_t m[KP];
+#pragma unroll
+    for (int p = 0; p < KP; ++p) m[p] = 0;
+    if constexpr (LPT > 0) {
+        for (int i = 0; i < LPT; ++i) list_merge(m, Ls + ((size_t)bt * TK_LISTS + sub * LPT + i) * KP);
+    }
+    __syncthreads();
+    uint64_t *Ms = Ls;   // [BT][TPS][KP]
+#pragma unroll
+    for (int p = 0; p < KP; ++p) Ms[((size_t)bt * TPS + sub) * KP + p] = m[p];
+    __syncthreads();
+    if (sub == 0 && bt < nb) {
+        for (int i = 1; i < TPS; ++i) list_merge(m, Ms + ((size_t)bt * TPS + i) * KP);
+        uint64_t *dst = a.part + ((size_t)(b0 + bt) * a.nwg + blockIdx.x) * KP;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) dst[p] = m[p];
+    }
+}
+
 template <int VT, int SPL, int KP>
 __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
     using T = typename TkVal<VT>::T;
@@ -342,18 +414,7 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
     const int b0 = blockIdx.y * BT;
     const int nb = min(BT, a.B - b0);
 
-    // stage the tile transposed, Xs[c*BT + b], with a zero column d and zero
-    // samples past B
-    {
-        T *Xs = reinterpret_cast<T *>(tk_smem);
-        const T *X = static_cast<const T *>(a.X) + (int64_t)b0 * d;
-        for (int b = 0; b < BT; ++b)
-            for (int c = tid; c <= d; c += TK_THREADS)
-                Xs[c * BT + b] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
-        for (int i = tid; i < BT * (1 + TK_LISTS); i += TK_THREADS)
-            reinterpret_cast<uint32_t *>(tk_smem + a.thr_off)[i] = 0u;
-    }
-    __syncthreads();
+    tk_stage<T, BT>(a, b0, nb);
 
     const int xl = u * SPL * (int)sizeof(T);   // LDS byte offset of this lane's samples of column 0
     // Per sample: the lane's sorted list, the score of its last entry once it
@@ -424,30 +485,8 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
                     const int64_t l = l0 + g;
                     const bool valid = l < a.L;
                     ++steps;
-                    if ((steps & (steps - 1)) == 0 || (steps & 63) == 0) {
-                        // every wave turns the list bests of 8 samples into
-                        // bounds, after 1, 2, 4, ... rows and then every 64
-                        if (lane < BT / TK_WAVES) {
-                            const int bt = wave * (BT / TK_WAVES) + lane;
-                            uint32_t best[KP];
-#pragma unroll
-                            for (int p = 0; p < KP; ++p) best[p] = 0u;
-                            for (int i = 0; i < TK_LISTS; ++i) {
-                                uint32_t v = __hip_atomic_load(lmax + bt * TK_LISTS + i, __ATOMIC_RELAXED,
-                                                               __HIP_MEMORY_SCOPE_WORKGROUP);
-#pragma unroll
-                                for (int p = 0; p < KP; ++p) {
-                                    const uint32_t hi = max(best[p], v), lo = min(best[p], v);
-                                    best[p] = hi;
-                                    v = lo;
-                                }
-                            }
-                            uint32_t vk = 0u;
-#pragma unroll
-                            for (int p = 0; p < KP; ++p) vk = p == a.K - 1 ? best[p] : vk;
-                            atomicMax(shared_thr + bt, vk);
-                        }
-                    }
+                    if ((steps & (steps - 1)) == 0 || (steps & 63) == 0)
+                        tk_list_bound<KP, BT>(lmax, shared_thr, a.K, wave, lane);
                     if ((steps & 3) == 0) {
                         // refresh the workgroup's bounds for this lane's samples
 #pragma unroll
@@ -497,27 +536,200 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
 #pragma unroll
         for (int p = 0; p < KP; ++p) dst[p] = kl[e][p];
     }
-    __syncthreads();
-    constexpr int TPS = TK_THREADS / BT;    // threads per sample
-    constexpr int LPT = TK_LISTS / TPS;     // lists per thread in the first stage
-    const int bt = tid / TPS, sub = tid % TPS;
-    uint64_t m[KP];
+    tk_merge_lists<KP, BT>(a, b0, nb);
+}
+
+// ---------------------------------------------------------------------------
+// k_topk_tr: the scan for bf16 values and fan-in 32 with transposing LDS
+// gathers (ds_read_b64_tr_b16).  The tile is the same [d+1][64] X tile, a
+// wave again serves 4 label rows per step, one per DPP row of 16 lanes, and a
+// lane keeps the lists of 4 samples; only the gather differs.
+//
+// ds_read_b64_tr_b16 reads 8 bytes per lane at the lane's own address and
+// hands them out transposed within each group of 16 lanes: lane 4m + t of
+// the group receives element t of the 8 bytes read by lanes m, m+4, m+8 and
+// m+12, in that order.  So when lane m + 4j reads samples 16m + 4p .. +3 of
+// the column of slot 4sq + j, lane 4m + t receives sample 16m + 4p + t of the
+// four slots 4sq .. 4sq+3: a slot-major quad that v_dot2 takes against the
+// row's weight pairs as stored, with no repacking.  Per row a lane issues 32
+// such reads (8 slot quads x 4 sample pieces p) and 64 dot2.
+//
+// In the wave's row group g the sample pieces are visited in the order p =
+// e ^ g (e = 0..3), so the 64 lanes of one read touch 16 distinct 8-byte
+// pieces (4 per column group); with one order for all groups they would touch
+// 4, and the LDS banks would serve them 8 deep.
+//
+// The rows' indices and weights are read straight from HBM with range-checked
+// buffer loads, TR_AHEAD steps ahead: lane m + 4j loads the 8 indices of
+// slots 4sq + j it gathers for (immediate offsets, no address arithmetic), and
+// every lane of a row its 16 weight pairs.
+constexpr int TR_AHEAD = 2;
+
+struct TrRow {
+    uint32_t c[8];    // columns of slots 4sq + j (sq = 0..7) as stored
+    uint32_t w[16];   // the row's weights, pairs (4sq, 4sq+1) and (4sq+2, 4sq+3)
+    float bias;
+};
+
+template <bool IDX16>
+__device__ __forceinline__ void tr_load(Rsrc rI, Rsrc rW, Rsrc rB, uint32_t l, int j, TrRow &r) {
+    if constexpr (IDX16) {
+        const uint32_t base = l * 64u + 2u * (uint32_t)j;
 #pragma unroll
-    for (int p = 0; p < KP; ++p) m[p] = 0;
-    if constexpr (LPT > 0) {
-        for (int i = 0; i < LPT; ++i) list_merge(m, Ls + ((size_t)bt * TK_LISTS + sub * LPT + i) * KP);
+        for (int sq = 0; sq < 8; ++sq) r.c[sq] = __builtin_amdgcn_raw_buffer_load_b16(rI, base + 8u * sq, 0, 0);
+    } else {
+        const uint32_t base = l * 128u + 4u * (uint32_t)j;
+#pragma unroll
+        for (int sq = 0; sq < 8; ++sq) r.c[sq] = ld32(rI, base + 16u * sq);
     }
-    __syncthreads();
-    uint64_t *Ms = Ls;   // [BT][TPS][KP]
 #pragma unroll
-    for (int p = 0; p < KP; ++p) Ms[((size_t)bt * TPS + sub) * KP + p] = m[p];
-    __syncthreads();
-    if (sub == 0 && bt < nb) {
-        for (int i = 1; i < TPS; ++i) list_merge(m, Ms + ((size_t)bt * TPS + i) * KP);
-        uint64_t *dst = a.part + ((size_t)(b0 + bt) * a.nwg + blockIdx.x) * KP;
-#pragma unroll
-        for (int p = 0; p < KP; ++p) dst[p] = m[p];
+    for (int i = 0; i < 4; ++i) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rW, l * 64u + 16u * i, 0, 0);
+        r.w[4 * i] = v[0];
+        r.w[4 * i + 1] = v[1];
+        r.w[4 * i + 2] = v[2];
+        r.w[4 * i + 3] = v[3];
     }
+    r.bias = ldf(rB, l * 4u);
+}
+
+typedef short tr_v4s __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 tr_read(uint32_t off) {
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    const tr_v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) tr_v4s *)((__attribute__((address_space(3))) unsigned char *)tk_smem +
+                                                      off));
+    return __builtin_bit_cast(uint2, v);
+}
+
+template <int KP, bool IDX16>
+__global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
+    extern __shared__ __align__(16) unsigned char tk_smem[];
+    constexpr int BT = 64, NS = 4;   // tile, samples per lane
+    constexpr uint32_t COL = BT * 2; // bytes per LDS column
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, q = lane & 15;
+    const int d = a.d;
+    const int b0 = blockIdx.y * BT;
+    const int nb = min(BT, a.B - b0);
+    tk_stage<uint16_t, BT>(a, b0, nb);
+
+    // as a gather source, lane q reads sample block ms of slot js of each quad;
+    // as a receiver it holds samples 16*(q >> 2) + 4p + (q & 3)
+    const int ms = q & 3, js = q >> 2;
+    int smp[NS];   // the sample of accumulator e (piece p = e ^ g)
+    uint32_t poff[NS];
+#pragma unroll
+    for (int e = 0; e < NS; ++e) {
+        smp[e] = 16 * (q >> 2) + 4 * (e ^ g) + (q & 3);
+        poff[e] = 32u * ms + 8u * (e ^ g);
+    }
+
+    uint64_t kl[NS][KP];
+    float thr[NS], thr_sh[NS];
+    bool full[NS];
+#pragma unroll
+    for (int e = 0; e < NS; ++e) {
+#pragma unroll
+        for (int p = 0; p < KP; ++p) kl[e][p] = 0;
+        thr[e] = -INFINITY;
+        thr_sh[e] = -INFINITY;
+        full[e] = false;
+    }
+    uint32_t *shared_thr = reinterpret_cast<uint32_t *>(tk_smem + a.thr_off);
+    uint32_t *lmax = shared_thr + BT;
+    const int my_list = wave * TK_ROWS + g;
+
+    const Rsrc rI = make_rsrc(a.I, (uint32_t)a.L * (IDX16 ? 64u : 128u));
+    const Rsrc rW = make_rsrc(a.W, (uint32_t)a.L * 64u);
+    const Rsrc rB = make_rsrc(a.bias, a.bias ? (uint32_t)a.L * 4u : 0u);
+    const uint32_t L = (uint32_t)a.L;
+    const uint32_t stride = gridDim.x * (uint32_t)TK_LISTS;
+    uint32_t l0 = (blockIdx.x * TK_WAVES + wave) * TK_ROWS;   // the wave's row group this step
+    TrRow ring[TR_AHEAD];
+#pragma unroll
+    for (int i = 0; i < TR_AHEAD; ++i) tr_load<IDX16>(rI, rW, rB, l0 + i * stride + g, js, ring[i]);
+    int steps = 0;
+    while (l0 < L) {
+#pragma unroll
+        for (int i = 0; i < TR_AHEAD; ++i) {
+            if (l0 < L) {   // uniform
+                TrRow cur = ring[i];
+                // rows past L read zeros (range-checked loads)
+                tr_load<IDX16>(rI, rW, rB, l0 + TR_AHEAD * stride + g, js, ring[i]);
+                // column byte offsets; an index outside [0, d) reads the zero column d
+                uint32_t cb[8];
+#pragma unroll
+                for (int sq = 0; sq < 8; ++sq) cb[sq] = min(cur.c[sq], (uint32_t)d) * COL;
+                float z[NS];
+#pragma unroll
+                for (int e = 0; e < NS; ++e) z[e] = 0.f;
+                // two halves of four slot quads: the 16 reads of a half are
+                // issued together, then their 32 products
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint2 xr[4][NS];
+#pragma unroll
+                    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+                        for (int e = 0; e < NS; ++e) xr[s4][e] = tr_read(cb[4 * h + s4] + poff[e]);
+#pragma unroll
+                    for (int s4 = 0; s4 < 4; ++s4) {
+                        const int sq = 4 * h + s4;
+#pragma unroll
+                        for (int e = 0; e < NS; ++e)
+                            z[e] = dot2(xr[s4][e].y, cur.w[2 * sq + 1], dot2(xr[s4][e].x, cur.w[2 * sq], z[e]));
+                    }
+                }
+
+                const uint32_t l = l0 + g;
+                const bool valid = l < L;
+                ++steps;
+                if ((steps & (steps - 1)) == 0 || (steps & 63) == 0)
+                    tk_list_bound<KP, BT>(lmax, shared_thr, a.K, wave, lane);
+                if ((steps & 3) == 0) {
+#pragma unroll
+                    for (int e = 0; e < NS; ++e)
+                        thr_sh[e] = key_score((uint64_t)__hip_atomic_load(shared_thr + smp[e], __ATOMIC_RELAXED,
+                                                                          __HIP_MEMORY_SCOPE_WORKGROUP)
+                                              << 32);
+                }
+#pragma unroll
+                for (int e = 0; e < NS; ++e) {
+                    const float ze = z[e] + cur.bias;
+                    // this lane's rows come in ascending label order, so a
+                    // score equal to its own last entry's loses the tie;
+                    // NaN never enters
+                    const bool hit = valid & (smp[e] < nb) & ((ze > thr[e]) | (!full[e] & (ze == ze))) &
+                                     (ze >= thr_sh[e]);
+                    if (__builtin_amdgcn_ballot_w64(hit) != 0) {
+                        if (hit) {
+                            list_insert(kl[e], score_key(ze, l));
+                            lmax[smp[e] * TK_LISTS + my_list] = (uint32_t)(kl[e][0] >> 32);
+                            full[e] = kl[e][KP - 1] != 0;
+                            if (full[e]) {
+                                thr[e] = key_score(kl[e][KP - 1]);
+                                atomicMax(shared_thr + smp[e], (uint32_t)(kl[e][KP - 1] >> 32));
+                            }
+                        }
+                    }
+                }
+                l0 += stride;
+            }
+        }
+    }
+
+    // merge the workgroup's 32 lists per sample into one
+    __syncthreads();   // the X tile is no longer read
+    uint64_t *Ls = reinterpret_cast<uint64_t *>(tk_smem);
+#pragma unroll
+    for (int e = 0; e < NS; ++e) {
+        uint64_t *dst = Ls + ((size_t)smp[e] * TK_LISTS + my_list) * KP;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) dst[p] = kl[e][p];
+    }
+    tk_merge_lists<KP, BT>(a, b0, nb);
 }
 
 // block-wide maximum of one key per thread (TK_MERGE_THREADS threads)
@@ -632,6 +844,15 @@ const void *pick_spl(int spl, int kp) {
     return spl == 4 ? pick_kp<VT, 4>(kp) : spl == 2 ? pick_kp<VT, 2>(kp) : pick_kp<VT, 1>(kp);
 }
 
+template <bool IDX16>
+const void *tr_kernel_i(int kp) {
+    return kp == 1 ? reinterpret_cast<const void *>(&k_topk_tr<1, IDX16>)
+         : kp == 4 ? reinterpret_cast<const void *>(&k_topk_tr<4, IDX16>)
+                   : reinterpret_cast<const void *>(&k_topk_tr<8, IDX16>);
+}
+
+const void *tr_kernel(int kp, bool idx16) { return idx16 ? tr_kernel_i<true>(kp) : tr_kernel_i<false>(kp); }
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
@@ -655,6 +876,8 @@ bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p) {
     p->lds = std::max((size_t)p->thr_off + sizeof(uint32_t) * p->bt * (1 + TK_LISTS),
                       (size_t)TK_THREADS * spl * p->kp * 8);
     p->scan = ly.vt == FFSL_BF16 ? pick_spl<FFSL_BF16>(spl, p->kp) : pick_spl<FFSL_F32>(spl, p->kp);
+    if (ly.vt == FFSL_BF16 && ly.k == 32 && spl == 4 && p->kp <= 8 && ly.L < ((int64_t)1 << 25))
+        p->scan = tr_kernel(p->kp, ly.idx16 != 0);
     if (!p->scan) return false;
     p->nwg = 0;
     p->part = 0;
