@@ -333,15 +333,22 @@ __device__ __forceinline__ void tk_round_full(const TkRound<VT> &c, int xl, floa
 
 // Stage the batch tile transposed, Xs[c*BT + b], with a zero column d and
 // zero samples past B, and clear the per-sample bounds and list bests.
-template <typename T, int BT>
+//
+// With SWZ (the transposing scan), the 8-byte pieces of samples 4p .. 4p+3
+// of column c sit at piece p ^ tr_swz(c) of the column.
+__device__ __forceinline__ int tr_swz(int c) { return (c >> 1) & 3; }
+
+template <typename T, int BT, bool SWZ = false>
 __device__ __forceinline__ void tk_stage(const TkArgs &a, int b0, int nb) {
     extern __shared__ __align__(16) unsigned char tk_smem[];
     const int tid = threadIdx.x, d = a.d;
     T *Xs = reinterpret_cast<T *>(tk_smem);
     const T *X = static_cast<const T *>(a.X) + (int64_t)b0 * d;
     for (int b = 0; b < BT; ++b)
-        for (int c = tid; c <= d; c += TK_THREADS)
-            Xs[c * BT + b] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
+        for (int c = tid; c <= d; c += TK_THREADS) {
+            const int pos = SWZ ? ((((b >> 2) ^ tr_swz(c)) << 2) | (b & 3)) : b;
+            Xs[c * BT + pos] = (b < nb && c < d) ? X[(int64_t)b * d + c] : T(0);
+        }
     for (int i = tid; i < BT * (1 + TK_LISTS); i += TK_THREADS)
         reinterpret_cast<uint32_t *>(tk_smem + a.thr_off)[i] = 0u;
     __syncthreads();
@@ -554,16 +561,19 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_scan(TkArgs a) {
 // row's weight pairs as stored, with no repacking.  Per row a lane issues 32
 // such reads (8 slot quads x 4 sample pieces p) and 64 dot2.
 //
-// In the wave's row group g the sample pieces are visited in the order p =
-// e ^ g (e = 0..3), so the 64 lanes of one read touch 16 distinct 8-byte
-// pieces (4 per column group); with one order for all groups they would touch
-// 4, and the LDS banks would serve them 8 deep.
+// Bank conflicts.  In the wave's row group g the sample pieces are visited
+// in the order p = e ^ g (e = 0..3), so the four groups of one read touch
+// different pieces.  Within a group, the 16 lanes read 4 pieces of each of 4
+// random columns; a column's bank half follows its parity, so two columns of
+// the same parity would land on the same banks.  The tile therefore keeps
+// piece p of column c at p ^ ((c >> 1) & 3): columns then collide only when
+// they agree in their three low bits.
 //
 // The rows' indices and weights are read straight from HBM with range-checked
-// buffer loads, TR_AHEAD steps ahead: lane m + 4j loads the 8 indices of
+// buffer loads, TR_AHEAD steps ahead (a ring in registers: 3 steps, 2 for
+// lists of 8, which hold 64 registers): lane m + 4j loads the 8 indices of
 // slots 4sq + j it gathers for (immediate offsets, no address arithmetic), and
 // every lane of a row its 16 weight pairs.
-constexpr int TR_AHEAD = 2;
 
 struct TrRow {
     uint32_t c[8];    // columns of slots 4sq + j (sq = 0..7) as stored
@@ -606,6 +616,7 @@ __device__ __forceinline__ uint2 tr_read(uint32_t off) {
 template <int KP, bool IDX16>
 __global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
     extern __shared__ __align__(16) unsigned char tk_smem[];
+    constexpr int TR_AHEAD = KP >= 8 ? 2 : 3;
     constexpr int BT = 64, NS = 4;   // tile, samples per lane
     constexpr uint32_t COL = BT * 2; // bytes per LDS column
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -613,7 +624,7 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
     const int d = a.d;
     const int b0 = blockIdx.y * BT;
     const int nb = min(BT, a.B - b0);
-    tk_stage<uint16_t, BT>(a, b0, nb);
+    tk_stage<uint16_t, BT, true>(a, b0, nb);
 
     // as a gather source, lane q reads sample block ms of slot js of each quad;
     // as a receiver it holds samples 16*(q >> 2) + 4p + (q & 3)
@@ -634,7 +645,7 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
 #pragma unroll
         for (int p = 0; p < KP; ++p) kl[e][p] = 0;
         thr[e] = -INFINITY;
-        thr_sh[e] = -INFINITY;
+        thr_sh[e] = smp[e] < nb ? -INFINITY : INFINITY;
         full[e] = false;
     }
     uint32_t *shared_thr = reinterpret_cast<uint32_t *>(tk_smem + a.thr_off);
@@ -651,39 +662,64 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
 #pragma unroll
     for (int i = 0; i < TR_AHEAD; ++i) tr_load<IDX16>(rI, rW, rB, l0 + i * stride + g, js, ring[i]);
     int steps = 0;
+    const int kk = a.K - 1;   // the entry whose score bounds this lane's list (K <= KP)
+
+    // column byte offsets of a ring entry (an index outside [0, d) reads the
+    // zero column d) and their piece swizzles
+    auto cols = [&](const TrRow &r, uint32_t(&cb)[8], uint32_t(&cx)[8]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int sq = 0; sq < 8; ++sq) {
+            const uint32_t c = min(r.c[sq], (uint32_t)d);
+            cb[sq] = c * COL;
+            cx[sq] = 8u * (uint32_t)tr_swz((int)c);
+        }
+    };
+    // the 16 transposing reads of slot quads 4h .. 4h+3
+    auto issue = [&](const uint32_t(&cb)[8], const uint32_t(&cx)[8], int h, uint2(&xr)[4][NS])
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+            for (int e = 0; e < NS; ++e) xr[s4][e] = tr_read(cb[4 * h + s4] + (poff[e] ^ cx[4 * h + s4]));
+    };
+    // their 32 products, the four samples' chains interleaved
+    auto mac = [&](const uint2(&xr)[4][NS], const TrRow &r, int h, float(&z)[NS]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const int sq = 4 * h + s4;
+#pragma unroll
+            for (int e = 0; e < NS; ++e) z[e] = dot2(xr[s4][e].x, r.w[2 * sq], z[e]);
+#pragma unroll
+            for (int e = 0; e < NS; ++e) z[e] = dot2(xr[s4][e].y, r.w[2 * sq + 1], z[e]);
+        }
+    };
+
+    // Software pipeline by half steps: the reads of the next half are in
+    // flight while the products of the current one run.  TR_AHEAD steps per
+    // iteration with no branch around the loads, so that each ring entry is
+    // reloaded in place right after its last use; a step past the wave's last
+    // row group reads zeros (range-checked loads) and selects nothing.
+    uint32_t cb[8], cx[8];
+    uint2 xa[4][NS], xb[4][NS];
+    cols(ring[0], cb, cx);
+    issue(cb, cx, 0, xa);
     while (l0 < L) {
 #pragma unroll
         for (int i = 0; i < TR_AHEAD; ++i) {
-            if (l0 < L) {   // uniform
-                TrRow cur = ring[i];
-                // rows past L read zeros (range-checked loads)
-                tr_load<IDX16>(rI, rW, rB, l0 + TR_AHEAD * stride + g, js, ring[i]);
-                // column byte offsets; an index outside [0, d) reads the zero column d
-                uint32_t cb[8];
-#pragma unroll
-                for (int sq = 0; sq < 8; ++sq) cb[sq] = min(cur.c[sq], (uint32_t)d) * COL;
+            {
+                const TrRow &cur = ring[i];
+                issue(cb, cx, 1, xb);
+                __builtin_amdgcn_sched_barrier(0);
                 float z[NS];
 #pragma unroll
                 for (int e = 0; e < NS; ++e) z[e] = 0.f;
-                // two halves of four slot quads: the 16 reads of a half are
-                // issued together, then their 32 products
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    uint2 xr[4][NS];
-#pragma unroll
-                    for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-                        for (int e = 0; e < NS; ++e) xr[s4][e] = tr_read(cb[4 * h + s4] + poff[e]);
-#pragma unroll
-                    for (int s4 = 0; s4 < 4; ++s4) {
-                        const int sq = 4 * h + s4;
-#pragma unroll
-                        for (int e = 0; e < NS; ++e)
-                            z[e] = dot2(xr[s4][e].y, cur.w[2 * sq + 1], dot2(xr[s4][e].x, cur.w[2 * sq], z[e]));
-                    }
-                }
+                mac(xa, cur, 0, z);
+                cols(ring[(i + 1) % TR_AHEAD], cb, cx);
+                issue(cb, cx, 0, xa);
+                __builtin_amdgcn_sched_barrier(0);
+                mac(xb, cur, 1, z);
 
-                const uint32_t l = l0 + g;
+                const uint32_t l = l0 + i * stride + g;
                 const bool valid = l < L;
                 ++steps;
                 if ((steps & (steps - 1)) == 0 || (steps & 63) == 0)
@@ -691,33 +727,49 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk_tr(TkArgs a) {
                 if ((steps & 3) == 0) {
 #pragma unroll
                     for (int e = 0; e < NS; ++e)
-                        thr_sh[e] = key_score((uint64_t)__hip_atomic_load(shared_thr + smp[e], __ATOMIC_RELAXED,
-                                                                          __HIP_MEMORY_SCOPE_WORKGROUP)
-                                              << 32);
+                        if (smp[e] < nb)
+                            thr_sh[e] = key_score((uint64_t)__hip_atomic_load(shared_thr + smp[e], __ATOMIC_RELAXED,
+                                                                              __HIP_MEMORY_SCOPE_WORKGROUP)
+                                                  << 32);
                 }
+                // Admission: this lane's rows come in ascending label order,
+                // so a score equal to its own K-th entry's loses the tie.
+                // Only the lane's best K can reach the sample's top K, so the
+                // K-th entry bounds the list (the entries after it are kept
+                // but no longer admit).  thr_sh is never NaN, so a NaN score
+                // fails the first compare; a sample past B has thr_sh = +inf.
+                float ze[NS];
+                bool hit[NS];
+                bool any = false;
 #pragma unroll
                 for (int e = 0; e < NS; ++e) {
-                    const float ze = z[e] + cur.bias;
-                    // this lane's rows come in ascending label order, so a
-                    // score equal to its own last entry's loses the tie;
-                    // NaN never enters
-                    const bool hit = valid & (smp[e] < nb) & ((ze > thr[e]) | (!full[e] & (ze == ze))) &
-                                     (ze >= thr_sh[e]);
-                    if (__builtin_amdgcn_ballot_w64(hit) != 0) {
-                        if (hit) {
-                            list_insert(kl[e], score_key(ze, l));
+                    ze[e] = z[e] + cur.bias;
+                    hit[e] = valid & (ze[e] >= thr_sh[e]) & ((ze[e] > thr[e]) | !full[e]);
+                    any |= hit[e];
+                }
+                if (__builtin_amdgcn_ballot_w64(any) != 0) {
+#pragma unroll
+                    for (int e = 0; e < NS; ++e) {
+                        if (hit[e]) {
+                            list_insert(kl[e], score_key(ze[e], l));
                             lmax[smp[e] * TK_LISTS + my_list] = (uint32_t)(kl[e][0] >> 32);
-                            full[e] = kl[e][KP - 1] != 0;
+                            uint64_t kth = kl[e][KP - 1];
+                            if (kk != KP - 1) {
+#pragma unroll
+                                for (int p = 0; p < KP - 1; ++p) kth = p == kk ? kl[e][p] : kth;
+                            }
+                            full[e] = kth != 0;
                             if (full[e]) {
-                                thr[e] = key_score(kl[e][KP - 1]);
-                                atomicMax(shared_thr + smp[e], (uint32_t)(kl[e][KP - 1] >> 32));
+                                thr[e] = key_score(kth);
+                                atomicMax(shared_thr + smp[e], (uint32_t)(kth >> 32));
                             }
                         }
                     }
                 }
-                l0 += stride;
             }
+            tr_load<IDX16>(rI, rW, rB, l0 + (i + TR_AHEAD) * stride + g, js, ring[i]);
         }
+        l0 += TR_AHEAD * stride;
     }
 
     // merge the workgroup's 32 lists per sample into one
@@ -844,10 +896,16 @@ const void *pick_spl(int spl, int kp) {
     return spl == 4 ? pick_kp<VT, 4>(kp) : spl == 2 ? pick_kp<VT, 2>(kp) : pick_kp<VT, 1>(kp);
 }
 
+// the transposing scan keeps lists of exactly 1, 3 or 5 entries for the
+// usual P@1, P@3 and P@5 (an insert costs one compare and select per entry),
+// and of 8 otherwise
+int tr_kp(int topk) { return topk == 1 ? 1 : topk <= 3 ? 3 : topk <= 5 ? 5 : 8; }
+
 template <bool IDX16>
 const void *tr_kernel_i(int kp) {
     return kp == 1 ? reinterpret_cast<const void *>(&k_topk_tr<1, IDX16>)
-         : kp == 4 ? reinterpret_cast<const void *>(&k_topk_tr<4, IDX16>)
+         : kp == 3 ? reinterpret_cast<const void *>(&k_topk_tr<3, IDX16>)
+         : kp == 5 ? reinterpret_cast<const void *>(&k_topk_tr<5, IDX16>)
                    : reinterpret_cast<const void *>(&k_topk_tr<8, IDX16>);
 }
 
@@ -876,8 +934,12 @@ bool topk_shape(const Layer &ly, int B, int topk, TopkPlan *p) {
     p->lds = std::max((size_t)p->thr_off + sizeof(uint32_t) * p->bt * (1 + TK_LISTS),
                       (size_t)TK_THREADS * spl * p->kp * 8);
     p->scan = ly.vt == FFSL_BF16 ? pick_spl<FFSL_BF16>(spl, p->kp) : pick_spl<FFSL_F32>(spl, p->kp);
-    if (ly.vt == FFSL_BF16 && ly.k == 32 && spl == 4 && p->kp <= 8 && ly.L < ((int64_t)1 << 25))
+    if (ly.vt == FFSL_BF16 && ly.k == 32 && spl == 4 && p->kp <= 8 && ly.L < ((int64_t)1 << 25)) {
+        p->kp = tr_kp(topk);
+        p->lds = std::max((size_t)p->thr_off + sizeof(uint32_t) * p->bt * (1 + TK_LISTS),
+                          (size_t)TK_THREADS * spl * p->kp * 8);
         p->scan = tr_kernel(p->kp, ly.idx16 != 0);
+    }
     if (!p->scan) return false;
     p->nwg = 0;
     p->part = 0;
@@ -924,7 +986,11 @@ int launch_topk(const Layer &ly, const void *X, int B, int topk, int32_t *top_la
     switch (p.kp) {
     case 1: hipLaunchKernelGGL(k_topk_merge<1>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
                                top_lab, top_sc, off, lab, rel); break;
+    case 3: hipLaunchKernelGGL(k_topk_merge<3>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                               top_lab, top_sc, off, lab, rel); break;
     case 4: hipLaunchKernelGGL(k_topk_merge<4>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
+                               top_lab, top_sc, off, lab, rel); break;
+    case 5: hipLaunchKernelGGL(k_topk_merge<5>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
                                top_lab, top_sc, off, lab, rel); break;
     case 8: hipLaunchKernelGGL(k_topk_merge<8>, dim3(B), dim3(TK_MERGE_THREADS), 0, st, a.part, p.nwg, topk,
                                top_lab, top_sc, off, lab, rel); break;

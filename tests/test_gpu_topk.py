@@ -44,7 +44,7 @@ CASES = {
     "c1_bigL": synth.scaled(W1["c1_fp32_L4096"], L=120000, B=16, name="c1_bigL"),
     "b16_bigL": synth.scaled(C4, L=90000, B=16, d=256, name="b16_bigL"),
 }
-TOPKS = {"c4s": [1, 5, 8, 16], "c4s_b100": [5], "c3s": [3, 16], "c1": [5, 12], "odd_k7": [2, 9],
+TOPKS = {"c4s": [1, 2, 3, 5, 7, 8, 16], "c4s_b100": [5], "c3s": [3, 16], "c1": [5, 12], "odd_k7": [2, 9],
          "k40_f32": [4], "b1": [1, 16], "c1_bigL": [4], "b16_bigL": [8]}
 
 
