@@ -344,6 +344,30 @@ __device__ __forceinline__ void tk_stage(const TkArgs &a, int b0, int nb) {
     const int tid = threadIdx.x, d = a.d;
     T *Xs = reinterpret_cast<T *>(tk_smem);
     const T *X = static_cast<const T *>(a.X) + (int64_t)b0 * d;
+    if constexpr (SWZ && BT == 64 && sizeof(T) == 2) {
+        if ((d & 7) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
+            // a wave takes 8 columns of its 64 samples: one 16-byte load per
+            // lane (lane = sample) and eight 2-byte LDS writes, which fall
+            // on distinct banks
+            const int lane = tid & 63;
+            for (int cc = tid >> 6; cc < d / 8; cc += TK_THREADS / 64) {
+                uint4 v = make_uint4(0u, 0u, 0u, 0u);
+                if (lane < nb) v = *reinterpret_cast<const uint4 *>(X + (int64_t)lane * d + 8 * cc);
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int c = 8 * cc + k;
+                    const int pos = (((lane >> 2) ^ tr_swz(c)) << 2) | (lane & 3);
+                    Xs[c * BT + pos] = (T)(w[k >> 1] >> (16 * (k & 1)));
+                }
+            }
+            if (tid < BT) Xs[d * BT + tid] = T(0);
+            for (int i = tid; i < BT * (1 + TK_LISTS); i += TK_THREADS)
+                reinterpret_cast<uint32_t *>(tk_smem + a.thr_off)[i] = 0u;
+            __syncthreads();
+            return;
+        }
+    }
     for (int b = 0; b < BT; ++b)
         for (int c = tid; c <= d; c += TK_THREADS) {
             const int pos = SWZ ? ((((b >> 2) ^ tr_swz(c)) << 2) | (b & 3)) : b;
