@@ -72,6 +72,8 @@ WsLayout ws_layout(int64_t L, int32_t d, int32_t k, int32_t vt, int32_t B_max, i
     if (w.has_xt) off = align256(off + sizeof(uint32_t) * 1024 * (size_t)passes);
     w.xt = off;
     if (w.has_xt) off = align256(off + sizeof(uint16_t) * (size_t)passes * pass_b * (size_t)d);
+    w.set_list = off;
+    if (mx) off = align256(off + sizeof(int32_t) * (size_t)(L + 1));
     w.total = off;
     return w;
 }

@@ -12,6 +12,8 @@
 //                           padded with 0xffffffff (a key that matches no row);
 //                           a label outside [0,L) becomes that padding key
 //   the others              XT[p][i][b] = X[p*PB + b][i], zero past B
+//   workgroup 0 also clears zero_word when given (the deferred-row count of a
+//   fused step+SET sweep)
 #include "sweep_dev.h"
 
 namespace ffsl {
@@ -31,6 +33,7 @@ struct BatchPrepArgs {
     int64_t L;
     uint32_t *keys;         // [passes][BP_KEYS]
     uint16_t *xt;           // [passes][d][PB]
+    int32_t *zero_word;     // set to 0 when given
 };
 
 template <int PB>
@@ -38,6 +41,7 @@ __global__ void __launch_bounds__(BP_THREADS) k_batch_prep(const BatchPrepArgs a
     constexpr int SB = PB == 64 ? 6 : 4;   // sample bits of a key
     static_assert((1 << SB) == PB, "pass width");
     const int tid = threadIdx.x;
+    if (blockIdx.x == 0 && tid == 0 && a.zero_word) *a.zero_word = 0;
     if ((int)blockIdx.x < a.nsort) {
         __shared__ uint32_t tg[BP_KEYS];
         __shared__ int32_t smp[BP_KEYS];
@@ -103,7 +107,8 @@ __global__ void __launch_bounds__(BP_THREADS) k_batch_prep(const BatchPrepArgs a
 }  // namespace
 
 int launch_batch_prep(const uint16_t *X, int32_t B, int32_t d, const int32_t *off, const int32_t *lab,
-                      int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, hipStream_t st) {
+                      int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, int32_t *zero_word,
+                      hipStream_t st) {
     if (B < 1 || B > 2 * BP_THREADS) return fail(FFSL_EINVAL, "batch prep: B = %d outside [1, %d]", B, 2 * BP_THREADS);
     BatchPrepArgs a{};
     a.X = X;
@@ -118,6 +123,7 @@ int launch_batch_prep(const uint16_t *X, int32_t B, int32_t d, const int32_t *of
     a.nsort = nnz <= BP_KEYS ? a.passes : 0;
     a.keys = keys;
     a.xt = xt;
+    a.zero_word = zero_word;
     const int64_t units = (int64_t)a.passes * (pass_b / 8) * d;
     const int tgrid = (int)std::min<int64_t>((units + BP_THREADS - 1) / BP_THREADS, 1024);
     const dim3 grid(a.nsort + tgrid);

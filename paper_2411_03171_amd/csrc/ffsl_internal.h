@@ -35,6 +35,8 @@ struct WsLayout {
                         // batch passes of the fused fast path (B_max > 64, k = 32)
     size_t keys;        // uint32 [passes][1024]: each pass's sorted positives
     size_t xt;          // bf16 [passes][d][pass width]: the batch transposed per pass
+    size_t set_list;    // int32 [1 + L]: the rows the fused step+SET sweep left
+                        // to SET on a row list (count first), fan-in-32 path
     bool has_partial;
     bool has_xt;        // the shape may take a fused fast path (keys, xt allocated)
     size_t total;
@@ -126,14 +128,18 @@ struct SweepCall {
 int launch_sweep(const SweepCall &c);
 // the fused fast paths' per-call batch preparation: sorted positives per pass
 // (when nnz <= 1024) and the batch transposed per pass (batch_prep.hip)
+// (and zero_word, when given, is set to 0: the deferred-row count of a fused
+// step+SET sweep that follows)
 int launch_batch_prep(const uint16_t *X, int32_t B, int32_t d, const int32_t *off, const int32_t *lab,
-                      int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, hipStream_t st);
+                      int32_t nnz, int64_t L, int pass_b, uint32_t *keys, uint16_t *xt, int32_t *zero_word,
+                      hipStream_t st);
 // what the fast sweeps read besides the layer and the call
 struct FastBufs {
     const int32_t *tgt_b;     // sample of each positive (used when nnz > 1024)
     const uint32_t *keys;     // [passes][1024] sorted positives (nnz <= 1024)
     const uint16_t *xt;       // [passes][d][pass width] transposed batch
     float *loss_part, *dx_part, *dwp, *dbp;
+    int32_t *set_list;        // [1 + L] rows left to SET on a row list (count first)
 };
 bool sweep_mx_eligible(const Layer &ly, int B, int mode);
 int launch_sweep_mx(const SweepCall &c, const FastBufs &fb, int *grid_out, int *passes_out);
@@ -144,6 +150,10 @@ int launch_adam(const Layer &ly, const AdamParams &p, hipStream_t st);
 // is ignored
 int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round,
                uint8_t *mask, int32_t *exhausted, hipStream_t st, bool threshold = false, float tau = 0.f);
+// SET on the rows of list (list[0] = count, rows from list[1]); results as
+// launch_set gives those rows
+int launch_set_rows(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_t *mask, int32_t *exhausted,
+                    const int32_t *list, hipStream_t st);
 int launch_validate(const Layer &ly, int32_t *bad_rows, hipStream_t st);
 int launch_adam_flat(void *p, int vt, const float *g, float *m, float *v, int64_t n, const AdamParams &ap,
                      int num_cu, hipStream_t st);

@@ -20,6 +20,7 @@
 // Rows whose tiles would leave one small workgroup per CU (a fan-in of 64, a
 // width of 2048, fp32 weights at d = 768) run k_set_reg instead, which holds
 // each row in one lane's registers; see set_launch_km.
+#include <algorithm>
 #include <type_traits>
 
 #include "sweep_dev.h"
@@ -339,13 +340,8 @@ __global__ void __launch_bounds__(SET_MAX_ROWS) k_set(const SetArgs a) {
 // the pruned slots as k_set does.  The draws, the selection and therefore
 // every result are those of k_set.
 template <int KM, int VT>
-__global__ void __launch_bounds__(SET_REG_ROWS) k_set_reg(const SetArgs a) {
-    // accepted columns beyond the first SET_REG_ACC of each row, [q][lane]
-    extern __shared__ uint32_t acc_lds[];
+__device__ __forceinline__ void set_reg_row(const SetArgs &a, int64_t l, uint32_t *acc_lds, int tid) {
     const int k = a.k, d = a.d;
-    const int tid = threadIdx.x;
-    const int64_t l = (int64_t)blockIdx.x * SET_REG_ROWS + tid;
-    if (l >= a.L) return;  // no block-level synchronisation below
 
     // the row: indices (slots past k hold a value no candidate equals) and
     // keys |W| (bf16: 15 bits, fp32: 31 bits)
@@ -599,6 +595,27 @@ __global__ void __launch_bounds__(SET_REG_ROWS) k_set_reg(const SetArgs a) {
     }
 }
 
+
+// acc_lds: accepted columns beyond the first SET_REG_ACC of each row,
+// [q][lane]; the rows need no block-level synchronisation
+template <int KM, int VT>
+__global__ void __launch_bounds__(SET_REG_ROWS) k_set_reg(const SetArgs a) {
+    extern __shared__ uint32_t acc_lds[];
+    const int64_t l = (int64_t)blockIdx.x * SET_REG_ROWS + threadIdx.x;
+    if (l < a.L) set_reg_row<KM, VT>(a, l, acc_lds, threadIdx.x);
+}
+
+// SET on the rows of a list (list[0] = their count, the rows from list[1]):
+// the rows whose first four regrowth draws the fused step+SET sweep could
+// not use; each row's result is the one k_set_reg gives it
+template <int KM, int VT>
+__global__ void __launch_bounds__(SET_REG_ROWS) k_set_reg_list(const SetArgs a, const int32_t *list) {
+    extern __shared__ uint32_t acc_lds[];
+    const int64_t n = list[0];
+    for (int64_t i = (int64_t)blockIdx.x * SET_REG_ROWS + threadIdx.x; i < n; i += (int64_t)gridDim.x * SET_REG_ROWS)
+        set_reg_row<KM, VT>(a, list[1 + i], acc_lds, threadIdx.x);
+}
+
 template <int KM>
 __global__ void __launch_bounds__(256) k_validate(const int32_t *I, int64_t L, int k, int d, int32_t *bad,
                                                   int idx16) {
@@ -696,6 +713,43 @@ int launch_set(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_
     a.round = round;
     a.cap = 64 * (int64_t)ly.k + 4096;
     return ly.vt == FFSL_BF16 ? set_launch_vt<FFSL_BF16>(a, st) : set_launch_vt<FFSL_F32>(a, st);
+}
+
+int launch_set_rows(const Layer &ly, int32_t n, uint64_t seed, uint64_t round, uint8_t *mask, int32_t *exhausted,
+                    const int32_t *list, hipStream_t st) {
+    if (ly.k > 64) return fail(FFSL_EUNSUPPORTED, "SET on a row list: fan-in %d", ly.k);
+    SetArgs a{};
+    a.L = ly.L;
+    a.d = ly.d;
+    a.k = ly.k;
+    a.n = n;
+    a.words = (ly.d + 31) / 32;
+    a.W = ly.W;
+    a.I = ly.I;
+    a.idx16 = ly.idx16;
+    a.m = ly.m;
+    a.v = ly.v;
+    a.mask = mask;
+    a.exhausted = exhausted;
+    a.seed = seed;
+    a.round = round;
+    a.cap = 64 * (int64_t)ly.k + 4096;
+    const size_t shm = sizeof(uint32_t) * (size_t)max(n - SET_REG_ACC, 0) * SET_REG_ROWS;
+    const void *kern;
+    if (ly.vt == FFSL_BF16)
+        kern = ly.k <= 32 ? reinterpret_cast<const void *>(&k_set_reg_list<32, FFSL_BF16>)
+                          : reinterpret_cast<const void *>(&k_set_reg_list<64, FFSL_BF16>);
+    else
+        kern = ly.k <= 32 ? reinterpret_cast<const void *>(&k_set_reg_list<32, FFSL_F32>)
+                          : reinterpret_cast<const void *>(&k_set_reg_list<64, FFSL_F32>);
+    hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return fail(FFSL_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    // a few workgroups per CU cover the rare deferred rows; with none the
+    // workgroups exit at once
+    const int blocks = (int)std::min<int64_t>((ly.L + SET_REG_ROWS - 1) / SET_REG_ROWS, (int64_t)ly.num_cu * 4);
+    hipLaunchKernelGGL(reinterpret_cast<void (*)(SetArgs, const int32_t *)>(const_cast<void *>(kern)), dim3(blocks),
+                       dim3(SET_REG_ROWS), shm, st, a, list);
+    return check_launch("set_update (deferred rows)");
 }
 
 int launch_validate(const Layer &ly, int32_t *bad, hipStream_t st) {

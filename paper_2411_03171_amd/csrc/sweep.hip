@@ -506,9 +506,13 @@ int launch_sweep(const SweepCall &c) {
         fb.dx_part = a.dx_part;
         fb.dwp = reinterpret_cast<float *>(ly.ws + wl.dwp);
         fb.dbp = reinterpret_cast<float *>(ly.ws + wl.dbp);
+        // the fan-in-32 path's list of rows left to SET on a row list, its
+        // count cleared by the batch preparation
+        fb.set_list = use_wide ? nullptr : reinterpret_cast<int32_t *>(ly.ws + wl.set_list);
         int rc = launch_batch_prep(static_cast<const uint16_t *>(c.X), B, d, c.tgt_off, c.tgt_lab, c.nnz, ly.L,
                                    use_wide ? WD_PASS_B : MX_PASS_B, reinterpret_cast<uint32_t *>(ly.ws + wl.keys),
-                                   reinterpret_cast<uint16_t *>(ly.ws + wl.xt), c.stream);
+                                   reinterpret_cast<uint16_t *>(ly.ws + wl.xt), c.set_n > 0 ? fb.set_list : nullptr,
+                                   c.stream);
         if (rc) return rc;
         int passes = 1;
         rc = use_wide ? launch_sweep_wide(c, fb, &grid, &passes) : launch_sweep_mx(c, fb, &grid, &passes);

@@ -83,10 +83,10 @@ struct MxArgs {
     float *dwp, *dbp;
     int32_t hinge;   // squared hinge instead of BCE
     // SET fused into the pass that applies Adam (see the SETF kernels)
-    int32_t set_n, set_cap;
+    int32_t set_n;
     uint64_t set_seed, set_round;
     uint8_t *set_mask;
-    int32_t *set_exhausted;
+    int32_t *set_list;   // rows left to SET on a row list: count, then the rows
     uint32_t nb_mask;
 };
 
@@ -97,7 +97,7 @@ struct Rsrcs {
     Rsrc XT, K, W, I, m, v, b, bm, bv, dwp, dbp, mk;
 };
 
-constexpr int MX_SET_NMAX = 8;   // pruned slots per row the fused SET handles
+constexpr int MX_SET_NMAX = 4;   // pruned slots per row the fused SET handles (its four draws ahead)
 constexpr int MX_SET_AHEAD = 8;  // chunks whose first candidates a wave draws at once
 
 // minimum of x over the 16 lanes of a DPP row, in every lane
@@ -460,24 +460,13 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
                         for (int q = 0; q < 4; ++q)
                             if (got < a.set_n) offer((int)cw[q]);
                     }
-                    // later attempts (a row that met a held column): drawn here
-                    uint64_t p0 = 0, p1 = 0, p2 = 0, p3 = 0;
-                    for (int att = 4; got < a.set_n && att < a.set_cap; ++att) {
-                        if ((att & 3) == 0) {
-                            p0 = (uint64_t)l;
-                            p1 = a.set_round;
-                            p2 = (uint64_t)(att >> 2);
-                            p3 = 0;
-                            philox4x64_10(p0, p1, p2, p3, a.set_seed, SET_KEY_HI);
-                        }
-                        const int ws = att & 3;
-                        const uint64_t word = ws == 0 ? p0 : ws == 1 ? p1 : ws == 2 ? p2 : p3;
-                        offer((int)__umul64hi(word, (uint64_t)d));
-                    }
-                    // a row that ran out of attempts keeps its slots
+                    // A row that met a held column among its first four draws
+                    // is left as the plain step leaves it and goes on a list
+                    // that SET then processes row by row (later draws are
+                    // rare, and drawing them here costs every row registers)
                     if (got < a.set_n) {
                         sel = 0;
-                        if (valid && u == 0 && a.set_exhausted) atomicAdd(a.set_exhausted, 1);
+                        if (valid && u == 0) a.set_list[1 + atomicAdd(a.set_list, 1)] = (int32_t)l;
                     }
                     // pruned slots restart at zero
                     if ((sel >> Kown) & 1u) {
@@ -665,11 +654,10 @@ int launch_sweep_mx(const SweepCall &c, const FastBufs &fb, int *grid_out, int *
     a.hinge = (c.flags & FFSL_LOSS_SQHINGE) ? 1 : 0;
     const bool setf = c.set_n >= 1 && c.set_n <= MX_SET_NMAX && sweep_mx_lds(ly.d, true) <= 160 * 1024;
     a.set_n = c.set_n;
-    a.set_cap = 64 * MX_K + 4096;
     a.set_seed = c.set_seed;
     a.set_round = c.set_round;
     a.set_mask = c.set_mask;
-    a.set_exhausted = c.set_exhausted;
+    a.set_list = fb.set_list;
     a.nb_mask = c.set_mask ? (uint32_t)(ly.L * MX_K) : 0u;
     a.nb_W = (uint32_t)(ly.L * MX_K * 2);
     a.idx16 = ly.idx16;
@@ -702,6 +690,12 @@ int launch_sweep_mx(const SweepCall &c, const FastBufs &fb, int *grid_out, int *
     if (ly.ev_stop) {
         hipError_t e = hipEventRecord(ly.ev_stop, c.stream);
         if (e != hipSuccess) return fail(FFSL_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    if (setf) {
+        // the rows whose first four draws did not suffice
+        int rc = launch_set_rows(ly, c.set_n, c.set_seed, c.set_round, c.set_mask, c.set_exhausted, fb.set_list,
+                                 c.stream);
+        if (rc) return rc;
     }
     *grid_out = grid;
     *passes_out = passes;
