@@ -93,7 +93,8 @@ FFSL_API int ffsl_version(void);
  * fused step carries dW and dbias between passes over the batch in 4*(L*k + L)
  * bytes: for k = 32, d a multiple of 128 up to 768, L < 2^25 and B_max > 64
  * (passes of 64 samples), and for k = 64, d a multiple of 128 up to 2048,
- * L < 2^24 and B_max > 16 (passes of 16).
+ * L < 2^24 and B_max > 16 (passes of 16).  The fan-in-32 shapes also hold a
+ * list of up to L row numbers (4*(L + 1) bytes) for ffsl_train_step_set.
  * Returns 0 for invalid shapes. */
 FFSL_API size_t ffsl_workspace_bytes(int64_t L, int32_t d, int32_t k, int32_t B_max,
                             int32_t nnz_max);
@@ -203,9 +204,12 @@ FFSL_API int ffsl_train_step(ffsl_layer *layer, const void *X, int32_t B,
  * as ffsl_train_step(...) and then ffsl_set_update(layer, frac, seed,
  * set_round, pruned_mask_out, exhausted_out) on the same stream (Sec. 2.1:
  * the prune-regrow cycle runs between training steps).  On the fused bf16
- * fan-in-32 path with at most 8 pruned slots per row the sweep that applies
- * Adam also selects, regrows and zero-initialises, and rewrites each row's
- * index words once; elsewhere the two calls run back to back.  The keys are
+ * fan-in-32 path with at most 4 pruned slots per row the sweep that applies
+ * Adam also selects, regrows from four draws per row made ahead, and
+ * zero-initialises, and rewrites each row's index words once; a row whose
+ * four draws do not suffice is left as the step leaves it and finished by a
+ * second kernel that runs SET on those rows only (their row numbers are kept
+ * in the workspace).  Elsewhere the two calls run back to back.  The keys are
  * those of the updated, stored weights.  Errors are those of both calls,
  * reported before anything is launched. */
 FFSL_API int ffsl_train_step_set(ffsl_layer *layer, const void *X, int32_t B,
