@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
 
 def sweep_source_hash():
     h = hashlib.sha256()
-    for name in ("sweep.hip", "sweep_mx.hip", "sweep_dev.h", "ffsl_internal.h"):
+    for name in ("sweep.hip", "sweep_mx.hip", "sweep_wide.hip", "batch_prep.hip", "sweep_dev.h", "ffsl_internal.h"):
         with open(os.path.join(ROOT, "paper_2411_03171_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -86,9 +86,10 @@ def set_bytes(w, value_bytes, n):
     return w.L * (w.k * (value_bytes + 4) + n * (4 + value_bytes + 8))
 
 
-def load_traffic(workload, src_hash):
-    """HBM traffic per launch measured with rocprofv3 counters, if the profile
-    was taken on the current sweep source; else None."""
+def load_traffic(workload, src_hash, key="bytes_per_launch"):
+    """HBM traffic measured with rocprofv3 counters (per launch of the main
+    sweep kernel, or per step over all batch passes), if the profile was taken
+    on the current sweep source; else None."""
     path = os.path.join(ROOT, "profiles", "sweep_fused_%s_traffic.json" % workload)
     if not os.path.exists(path):
         return None
@@ -96,7 +97,7 @@ def load_traffic(workload, src_hash):
         t = json.load(f)
     if t.get("source_hash") != src_hash:
         return None
-    return t.get("bytes_per_launch")
+    return t.get(key)
 
 
 def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
@@ -231,8 +232,18 @@ def time_composed(torch, ffsl, synth, ev, stream, dev, reps, seed):
             Xs = X
         ms = median_ms(lambda t: model.train_step(X, off, lab, t))
         ms_sparse = median_ms(lambda t: layer.train_step(Xs, off, lab, t))
+        # the sparse layer's step against the HBM roofline: every [L,k] array
+        # once (as for the main workload); traffic from the counters when a
+        # profile of the current source holds it (bytes per step, all passes)
+        sb = fused_step_bytes(w, 2 if w.value == "bf16" else 4)
+        sgbs = sb / (ms_sparse * 1e-3) / 1e9
+        straffic = load_traffic(w.name, sweep_source_hash(), key="bytes_per_step")
         out[name] = {"ms_median": ms, "sparse_ms_median": ms_sparse, "dense_parts_ms": ms - ms_sparse,
                      "value": w.B * w.L / (ms * 1e-3), "unit": "sample*labels/s",
+                     "sparse_roofline": {"bound": "hbm", "achieved": sgbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                         "frac": sgbs / HBM_PEAK_GBS, "algorithmic_bytes": sb,
+                                         "traffic": straffic,
+                                         "note": "whole sparse step (all batch passes, dX reduction) timed"},
                      "shape": {"L": w.L, "k": w.k, "B": w.B, "d": w.d, "din": w.din,
                                "aux_clusters": w.aux_clusters}}
         print("[bench] composed step %s: %.3f ms (sparse layer alone %.3f ms)" % (name, ms, ms_sparse),
