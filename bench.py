@@ -175,8 +175,8 @@ def time_dense_parts(torch, ffsl, synth, ev, stream, dev, reps):
                                              ws5.numel(), stream))
     us = median_us(aux_step)
     flops = 3 * 2.0 * B * d * C
-    # Wa read twice, dWa written, dZ written and read in fp32 and bf16
-    byts = 2 * d * C * 2 + d * C * 4 + B * C * (4 + 4 + 2 + 2 + 2)
+    # Wa read twice, dWa written, the bf16 dlogits written once and read by both products
+    byts = 2 * d * C * 2 + d * C * 4 + B * C * (2 + 2 + 2)
     out["aux_head"] = {"shape": {"B": B, "d": d, "C": C}, "us_median": us,
                        "flops": flops, "tflops": flops / (us * 1e-6) / 1e12, "mfma_peak_tflops": 2500.0,
                        "algorithmic_bytes": byts, "gbs": byts / (us * 1e-6) / 1e9}

@@ -14,8 +14,9 @@
 // layout), and the next 128-deep tiles are loaded into registers while the
 // matrix cores work on the current ones.  Long K (the dX products) is split
 // over blockIdx.z into fp32 partials that a second kernel sums in a fixed
-// order; so is the auxiliary head's forward, whose tiles alone would leave
-// most CUs idle, and its BCE runs in the kernel that sums the partials.
+// order.  The auxiliary head's forward runs in one pass over K with its BCE
+// in the epilogue: each workgroup marks its rows' cluster targets in LDS and
+// writes the bf16 dlogits, its column sums of them and its loss sum.
 #include <math.h>
 
 #include <algorithm>
@@ -33,7 +34,7 @@ constexpr int GT = 64;        // tile edge in M and N
 constexpr int GK = 128;       // K per stage
 constexpr int GKP = GK + 8;   // LDS row in elements (padded against bank conflicts)
 
-enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2 };
+enum Epi { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_GELU = 2, EPI_BCE = 3 };
 
 struct GemmArgs {
     const uint16_t *A;
@@ -42,8 +43,18 @@ struct GemmArgs {
     int64_t ldb;
     int M, N, K, kchunk;
     float *C;                 // STORE: C[m*N+n]; PARTIAL: C[(z*M+m)*N+n]; GELU: pre-activation
-    const float *bias;        // GELU: per-column bias (nullable)
-    uint16_t *H;              // GELU: bf16 activation
+    const float *bias;        // GELU, BCE: per-column bias (nullable)
+    uint16_t *H;              // GELU: bf16 activation; BCE: bf16 dlogits [M,N]
+    // BCE (the auxiliary head, M = samples, N = clusters): targets as CSR
+    // over the rows, label l counting for cluster l mod N when 0 <= l <
+    // n_labels; dlogit g = sc (sigmoid(z) - y); per workgroup, the column
+    // sums of g over its rows go to csum_part[blockIdx.y][n] and sc times its
+    // loss sum to loss_part[blockIdx.y * gridDim.x + blockIdx.x]; the logits
+    // to C when C is not null
+    const int32_t *off, *lab;
+    int64_t n_labels;
+    float sc;
+    float *csum_part, *loss_part;
 };
 
 // One operand's 64-row x 128-deep tile in flight: four 16-byte groups per
@@ -112,6 +123,30 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // BCE: bit j of ym[r] iff a positive of sample m0 + r falls in cluster n0 + j
+    __shared__ unsigned long long ym[EPI == EPI_BCE ? GT : 1];
+    if constexpr (EPI == EPI_BCE) {
+        if (tid < GT) ym[tid] = 0ull;
+        __syncthreads();
+        const int r1 = min(g.M, m0 + GT);
+        const int e0 = g.off[m0], e1 = g.off[r1];
+        for (int e = e0 + tid; e < e1; e += 256) {
+            const int l = g.lab[e];
+            if (l < 0 || l >= g.n_labels) continue;
+            const int cc = l % g.N - n0;
+            if (cc < 0 || cc >= GT) continue;
+            // the sample of entry e: the last row r with off[m0 + r] <= e
+            int lo = 0, hi = r1 - m0 - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (g.off[m0 + mid] <= e) lo = mid;
+                else hi = mid - 1;
+            }
+            atomicOr(&ym[lo], 1ull << cc);
+        }
+        __syncthreads();
+    }
+
     Tile ta, tb;
     load_tile<!TA>(ta, g.A, g.lda, m0, g.M, kbeg, kend, tid);
     load_tile<TB>(tb, g.B, g.ldb, n0, g.N, kbeg, kend, tid);
@@ -140,6 +175,52 @@ __global__ void __launch_bounds__(256) k_gemm(const GemmArgs g) {
                         __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mi], bv[ni], acc[mi][ni], 0, 0, 0);
         }
         __syncthreads();
+    }
+
+    if constexpr (EPI == EPI_BCE) {
+        // z = acc + bias, its BCE term and dlogit; the column sums of g over
+        // the tile's rows: each thread's rows, then the four lane groups of
+        // a wave, then the two waves of a column half, in that order
+        float csum[2] = {0.f, 0.f};
+        float lsum = 0.f;
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+            const int nl = 32 * wn + 16 * ni + col, n = n0 + nl;
+            const float bn = (g.bias && n < g.N) ? g.bias[n] : 0.f;
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int ml = 32 * wm + 16 * mi + 4 * kq + r, m = m0 + ml;
+                    if (m >= g.M || n >= g.N) continue;
+                    const float z = acc[mi][ni][r] + bn;
+                    const float y = ((ym[ml] >> nl) & 1ull) ? 1.f : 0.f;
+                    const float ex = expf(-fabsf(z));
+                    lsum += fmaxf(z, 0.f) - z * y + log1pf(ex);
+                    const float sig = z >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
+                    const float gg = g.sc * (sig - y);
+                    const int64_t o = (int64_t)m * g.N + n;
+                    g.H[o] = f32_to_bf16_bits(gg);
+                    if (g.C) g.C[o] = z;
+                    csum[ni] += gg;
+                }
+        }
+        __shared__ float cred[2][GT];
+        __shared__ float lred[4];
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+            csum[ni] += __shfl_xor(csum[ni], 16);
+            csum[ni] += __shfl_xor(csum[ni], 32);
+            if (kq == 0) cred[wm][32 * wn + 16 * ni + col] = csum[ni];
+        }
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) lsum += __shfl_xor(lsum, sh);
+        if (lane == 0) lred[wave] = lsum;
+        __syncthreads();
+        if (tid < GT && n0 + tid < g.N) g.csum_part[(int64_t)blockIdx.y * g.N + n0 + tid] = cred[0][tid] + cred[1][tid];
+        if (tid == 0)
+            g.loss_part[blockIdx.y * gridDim.x + blockIdx.x] = g.sc * ((lred[0] + lred[1]) + (lred[2] + lred[3]));
+        return;
     }
 
     // accumulator element r of tile (mi, ni) is C[row 4*kq + r][column col]
@@ -211,84 +292,6 @@ __global__ void __launch_bounds__(256) k_gelu_bwd_cols(const float *A, const flo
         }
     }
     column_sum_out(red, sum, c, rg, n, N, dc);
-}
-
-// The auxiliary head's forward epilogue over split-K partials: per element
-// z = ca[c] + sum_s P[s][b][c] (ascending s), its BCE term and dlogit
-// g = s (sigmoid(z) - y); g is stored in bf16 for the two products and the
-// logits go to Zout when asked.  A workgroup takes 32 columns of one block of
-// 32 rows (blockIdx.y) and writes that block's column sums of g to
-// csum_part[blockIdx.y][.] and its loss sum to
-// loss_part[blockIdx.y * gridDim.x + blockIdx.x]; k_col_parts then adds the
-// blocks in order.
-constexpr int BCE_ROWS = 32;
-__global__ void __launch_bounds__(256) k_bce_cols(const float *P, int S, int B, int N, const float *bias,
-                                                  const int32_t *off, const int32_t *lab, int64_t n_labels,
-                                                  float sc, uint16_t *G16,
-                                                  float *csum_part, float *Zout, float *loss_part) {
-    __shared__ float red[8][33];
-    __shared__ float lred[256];
-    __shared__ uint32_t ym[BCE_ROWS];   // targets of the block's rows in this workgroup's 32 clusters
-    const int c = threadIdx.x & 31, rg = threadIdx.x >> 5;
-    const int n = blockIdx.x * 32 + c;
-    const int64_t MN = (int64_t)B * N;
-    const int rb0 = blockIdx.y * BCE_ROWS, rb1 = min(B, rb0 + BCE_ROWS);
-    // cluster targets: bit c of ym[r] iff some positive l of sample rb0 + r has
-    // l mod N == blockIdx.x * 32 + c (labels outside [0, n_labels) are ignored)
-    if (threadIdx.x < BCE_ROWS) ym[threadIdx.x] = 0u;
-    __syncthreads();
-    {
-        const int e0 = off[rb0], e1 = off[rb1];
-        for (int e = e0 + (int)threadIdx.x; e < e1; e += 256) {
-            const int l = lab[e];
-            if (l < 0 || l >= n_labels) continue;
-            const int cc = l % N - blockIdx.x * 32;
-            if (cc < 0 || cc >= 32) continue;
-            int r = 0;   // the sample of entry e: the last row with off[row] <= e
-            while (rb0 + r + 1 < rb1 && off[rb0 + r + 1] <= e) ++r;
-            atomicOr(&ym[r], 1u << cc);
-        }
-    }
-    __syncthreads();
-    float sum = 0.f, lsum = 0.f;
-    if (n < N) {
-        const float bn = bias ? bias[n] : 0.f;
-        for (int b0 = rb0 + rg; b0 < rb1; b0 += 64) {
-            float zv[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) zv[i] = 0.f;
-            for (int sp = 0; sp < S; ++sp) {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    const int b = b0 + 8 * i;
-                    if (b < rb1) zv[i] += P[sp * MN + (int64_t)b * N + n];
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int b = b0 + 8 * i;
-                if (b < rb1) {
-                    const float z = zv[i] + bn;
-                    const float y = ((ym[b - rb0] >> c) & 1u) ? 1.f : 0.f;
-                    const float ex = expf(-fabsf(z));
-                    lsum += fmaxf(z, 0.f) - z * y + log1pf(ex);
-                    const float sig = z >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
-                    const float g = sc * (sig - y);
-                    const int64_t o = (int64_t)b * N + n;
-                    G16[o] = f32_to_bf16_bits(g);
-                    if (Zout) Zout[o] = z;
-                    sum += g;
-                }
-            }
-        }
-    }
-    lred[threadIdx.x] = lsum;
-    column_sum_out(red, sum, c, rg, n, N, csum_part + (int64_t)blockIdx.y * N);
-    for (int st = 128; st > 0; st >>= 1) {
-        if ((int)threadIdx.x < st) lred[threadIdx.x] += lred[threadIdx.x + st];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) loss_part[blockIdx.y * gridDim.x + blockIdx.x] = sc * lred[0];
 }
 
 // out[n] = sum_r part[r][n] over R row blocks, in order (out nullable); the
@@ -411,17 +414,13 @@ AuxWs aux_ws(int B_max, int d, int C) {
     AuxWs w{};
     int S, kc;
     split_k(C, &S, &kc);
-    int Sf, kcf;
-    split_fwd(d, (C + GT - 1) / GT * ((B_max + GT - 1) / GT), &Sf, &kcf);
     size_t off = 0;
-    w.zpart = off;
-    off = al256(off + sizeof(float) * (size_t)Sf * B_max * C);
     w.dz16 = off;
     off = al256(off + sizeof(uint16_t) * (size_t)B_max * C);
     w.loss_part = off;
-    off = al256(off + sizeof(float) * (size_t)((C + 31) / 32) * ((B_max + 31) / 32));
+    off = al256(off + sizeof(float) * (size_t)((C + GT - 1) / GT) * ((B_max + GT - 1) / GT));
     w.csum_part = off;
-    off = al256(off + sizeof(float) * (size_t)((B_max + 31) / 32) * C);
+    off = al256(off + sizeof(float) * (size_t)((B_max + GT - 1) / GT) * C);
     w.dx_part = off;
     off = al256(off + sizeof(float) * (size_t)S * B_max * d);
     w.total = off;
@@ -510,11 +509,10 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, int64_t n_labels, con
     uint16_t *dz16 = reinterpret_cast<uint16_t *>(ws + w.dz16);
     float *lp = reinterpret_cast<float *>(ws + w.loss_part);
     int rc;
-    // Za = X Wa + ca: split-K partials, A(m=b, k=i) = X[b*d+i], B(k=i, n=c) = Wa[i*C+c],
-    // then the BCE epilogue with the bf16 dlogits and their column sums
-    int Sf, kcf;
-    split_fwd(d, (C + GT - 1) / GT * ((B + GT - 1) / GT), &Sf, &kcf);
-    float *zp = reinterpret_cast<float *>(ws + w.zpart);
+    // Za = X Wa + ca in one pass over K, A(m=b, k=i) = X[b*d+i], B(k=i, n=c) = Wa[i*C+c],
+    // with the BCE epilogue: the bf16 dlogits, their column sums per row block
+    // of 64 and the loss per workgroup
+    float *cp = reinterpret_cast<float *>(ws + w.csum_part);
     GemmArgs g{};
     g.A = X;
     g.lda = d;
@@ -523,17 +521,19 @@ int launch_aux_bce(const uint16_t *X, int B, int d, int C, int64_t n_labels, con
     g.M = B;
     g.N = C;
     g.K = d;
-    g.kchunk = kcf;
-    g.C = zp;
-    rc = gemm<false, false, EPI_PARTIAL>(g, Sf, st);
+    g.kchunk = (d + GK - 1) / GK * GK;
+    g.C = Zout;
+    g.bias = ca;
+    g.H = dz16;
+    g.off = off;
+    g.lab = lab;
+    g.n_labels = n_labels;
+    g.sc = s;
+    g.csum_part = cp;
+    g.loss_part = lp;
+    rc = gemm<false, false, EPI_BCE>(g, 1, st);
     if (rc) return rc;
-    const int eblocks = (C + 31) / 32, rblocks = (B + BCE_ROWS - 1) / BCE_ROWS;
-    float *cp = reinterpret_cast<float *>(ws + w.csum_part);
-    hipLaunchKernelGGL(k_bce_cols, dim3(eblocks, rblocks), dim3(256), 0, st, zp, Sf, B, C, ca, off, lab, n_labels,
-                       s, dz16,
-                       cp, Zout, lp);
-    rc = check_launch("bce_cols");
-    if (rc) return rc;
+    const int eblocks = (C + GT - 1) / GT, rblocks = (B + GT - 1) / GT;
     if (dca || loss) {
         hipLaunchKernelGGL(k_bce_finish, dim3((C + 255) / 256), dim3(256), 0, st, cp, rblocks, C, dca, lp,
                            eblocks * rblocks, loss, accum_loss ? 1 : 0);

@@ -196,10 +196,9 @@ struct DenseWs {
 };
 // workspace of the auxiliary head
 struct AuxWs {
-    size_t zpart;      // fp32 [splits, B_max, C] split-K partials of the logits
     size_t dz16;       // bf16 [B_max, C] dlogits
-    size_t loss_part;  // fp32, one per epilogue workgroup (32 clusters x 32 samples)
-    size_t csum_part;  // fp32 [ceil(B_max/32), C] column sums of the dlogits per row block
+    size_t loss_part;  // fp32, one per forward workgroup (64 samples x 64 clusters)
+    size_t csum_part;  // fp32 [ceil(B_max/64), C] column sums of the dlogits per row block
     size_t dx_part;    // fp32 [splits, B_max, d]
     size_t total;
 };
