@@ -620,17 +620,28 @@ def main():
         torch.cuda.synchronize()
         im = sorted(one_step(lambda: layer.infer_topk(X, K_INF, off, lab, workspace=ws_inf))
                     for _ in range(args.infer_reps))
-        inf_ms = im[len(im) // 2]
+        single_ms = im[len(im) // 2]
+
+        # back-to-back calls between two events, as a serving loop issues them
+        # (the timed training steps run the same way): the host's setup of a
+        # call overlaps the previous call's kernels
+        def infer_calls():
+            for _ in range(args.infer_reps):
+                layer.infer_topk(X, K_INF, off, lab, workspace=ws_inf)
+        inf_ms = one_step(infer_calls) / args.infer_reps
         inf_bytes = w.L * w.k * (vb + 4) + 4 * w.L + w.B * w.d * vb
         inf_gbs = inf_bytes / (inf_ms * 1e-3) / 1e9
         # every (label row, slot, sample) reads one X value from LDS
         lds_bytes = w.L * w.k * w.B * vb
-        infer = {"topk": K_INF, "ms_median": inf_ms, "algorithmic_bytes": inf_bytes, "achieved": inf_gbs,
+        infer = {"topk": K_INF, "ms_per_call": inf_ms, "calls": args.infer_reps,
+                 "ms_median_single_call": single_ms, "algorithmic_bytes": inf_bytes, "achieved": inf_gbs,
                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": inf_gbs / HBM_PEAK_GBS,
                  "lds_gather_bytes": lds_bytes,
                  "sample_labels_per_s": w.B * w.L / (inf_ms * 1e-3)}
-        print("[bench] inference top-%d: %.3f ms median, %.0f GB/s algorithmic (%.1f%% of HBM peak)" %
-              (K_INF, inf_ms, inf_gbs, 100 * inf_gbs / HBM_PEAK_GBS), file=sys.stderr, flush=True)
+        print("[bench] inference top-%d: %.3f ms per call over %d back-to-back calls (%.3f ms median of single "
+              "calls), %.0f GB/s algorithmic (%.1f%% of HBM peak)" %
+              (K_INF, inf_ms, args.infer_reps, single_ms, inf_gbs, 100 * inf_gbs / HBM_PEAK_GBS),
+              file=sys.stderr, flush=True)
 
     # the same layer with 16-bit indices (2 bytes per slot less): the fused
     # step and the inference call
