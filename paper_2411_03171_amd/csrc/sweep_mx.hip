@@ -551,12 +551,23 @@ __global__ void __launch_bounds__(MX_THREADS, 1) k_sweep_mx(const MxArgs a) {
         }
     };
 
-    // two chunks per iteration, so the prefetch buffers swap roles instead of
-    // being copied (a copy would wait for the loads in flight)
-    for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += 2 * (int64_t)gridDim.x) {
-        step(chunk, pa, pb);
-        if (chunk + gridDim.x >= a.nchunks) break;
-        step(chunk + gridDim.x, pb, pa);
+    if constexpr (SETF) {
+        // one chunk per iteration, the next chunk's registers copied at the
+        // end of the step (its loads have landed by then): with SET's state
+        // the two-chunk body below exceeds the registers and spills, this one
+        // does not
+        for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += gridDim.x) {
+            step(chunk, pa, pb);
+            pa = pb;
+        }
+    } else {
+        // two chunks per iteration, so the prefetch buffers swap roles instead
+        // of being copied (a copy would wait for the loads in flight)
+        for (int64_t chunk = blockIdx.x; chunk < a.nchunks; chunk += 2 * (int64_t)gridDim.x) {
+            step(chunk, pa, pb);
+            if (chunk + gridDim.x >= a.nchunks) break;
+            step(chunk + gridDim.x, pb, pa);
+        }
     }
 
     // write this workgroup's dX partial [B][d]
