@@ -34,7 +34,7 @@
 //      full dW of slots Kp(u) + 2u0 and the next one;
 //   5. Adam on those two slots, streaming W, m, v back to HBM;
 //   6. dX: g and the old weights go to G and T, and the matrix cores add
-//      G x T^T (64 x 32 by 32 x d) into a per-workgroup dX held in AGPRs for
+//      G x T^T (64 x 32 by 32 x d) into a per-workgroup dX held in registers for
 //      the workgroup's whole life; it is written out once at the end.
 // The next chunk's index and weight rows are loaded into registers while the
 // current chunk computes; the matrix-core work of a chunk overlaps the VALU
